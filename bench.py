@@ -1,0 +1,202 @@
+"""Decode-attention bench: split-KV GQA sweep + LSE combine over every layer of a workload.
+
+One step = for every layer: qf_attn_decode_split (sweep of all cached K/V, per-shard (O, ln Z))
+then qf_attn_combine (merge to bf16 out + fp32 lse).  All layers' inputs are resident in HBM
+before the timed region.  Prints ONE JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, 8 TB/s
+DEFAULT_WORKLOAD = "qwen3-0.6b_b32_n32768_s64_l28"
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(case):
+    """Minimal HBM bytes of one sweep launch and one combine launch.
+
+    sweep: every cached position's K and V (2 * Hkv * D * 2 B), the block-table entry of every
+    used page (4 B), the queries (B * Hq * D * 2 B), the two int32 per request, and the partials
+    written for non-empty shards (Hq * (D + 1) * 4 B each).
+    combine: those partials read once, plus the bf16 out and fp32 lse written.
+    """
+    import numpy as np
+
+    B, Hq, Hkv, D = case.shape
+    n = case.ctx_lens.cpu().numpy().astype(np.int64)
+    S = case.n_shards.cpu().numpy().astype(np.int64)
+    pages = -(-n // 16)
+    per = np.where(pages > 0, -(-pages // np.maximum(S, 1)), 0)
+    live = np.where(per > 0, -(-pages // np.maximum(per, 1)), 0)   # non-empty shards
+    kv = int(n.sum()) * 2 * Hkv * D * 2
+    partials = int(live.sum()) * Hq * (D + 1) * 4
+    sweep = kv + int(pages.sum()) * 4 + B * Hq * D * 2 + B * 8 + partials
+    combine = partials + B * Hq * (D * 2 + 4)
+    return dict(kv=kv, sweep=sweep, combine=combine, attended=int(n.sum()))
+
+
+def cpu_baseline(cases, budget_s=15.0):
+    """The fp64 oracle (sweep per shard + pairwise merge) timed on the host over a bounded sample:
+    whole requests of the first layer, added until about ``budget_s`` of CPU work.  Device-to-host
+    copies are excluded from the timing."""
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_info
+
+    import oracle
+
+    case = cases[0]
+    B, Hq, Hkv, D = case.shape
+    ctx = case.ctx_lens.cpu().numpy()
+    S = case.n_shards.cpu().numpy()
+    bt = case.block_table.cpu().numpy()
+    q = case.q.double().cpu().numpy()
+    done_bytes, spent, reqs = 0, 0.0, 0
+    order = np.argsort(ctx)[::-1] if len(ctx) > 1 else [0]
+    for b in order:
+        npg = -(-int(ctx[b]) // 16)
+        idx = torch.as_tensor(bt[b, :npg], dtype=torch.long, device=case.k_cache.device)
+        k = case.k_cache.index_select(0, idx).float().cpu().numpy()
+        v = case.v_cache.index_select(0, idx).float().cpu().numpy()
+        table = np.arange(npg)[None, :]
+        t0 = time.perf_counter()
+        po, pl = oracle.decode_split(q[b:b + 1], k, v, table, ctx[b:b + 1], S[b:b + 1],
+                                     case.scale, int(S[b]))
+        oracle.fold_combine(po, pl)
+        spent += time.perf_counter() - t0
+        done_bytes += int(ctx[b]) * 2 * Hkv * D * 2
+        reqs += 1
+        if spent >= budget_s:
+            break
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {"value": done_bytes / spent / 1e9, "unit": "GB/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{reqs} whole request(s) of layer 0 ({done_bytes / 1e6:.0f} MB of KV, all "
+                      f"{Hq} heads, per-shard partials + pairwise merge), {spent:.1f} s; host has "
+                      f"{len(os.sched_getaffinity(0))} usable cores"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--layers", type=int, default=None,
+                    help="resident layers (default: the workload's own count)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(position sharding across GPUs is a design note, not code).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2608_15473_amd as qf
+    from workloads import WORKLOADS, workload_case
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    qf.load_library()
+    dev = torch.device("cuda:0")
+    w = WORKLOADS[args.workload]
+    L = args.layers or w.layers
+    log(f"[bench] generating {L} layer(s) of {w.name} on {torch.cuda.get_device_name(0)}")
+    t0 = time.time()
+    cases = [workload_case(w.name, layer=l, device=dev) for l in range(L)]
+    torch.cuda.synchronize()
+    log(f"[bench] inputs resident in {time.time() - t0:.1f} s")
+    B, Hq, Hkv, D = cases[0].shape
+    S = cases[0].max_shards
+    ab = [algorithmic_bytes(c) for c in cases]
+
+    po = torch.empty((B, S, Hq, D), dtype=torch.float32, device=dev)
+    pl = torch.empty((B, S, Hq), dtype=torch.float32, device=dev)
+    out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+    desc = qf.make_desc(cases[0].q, cases[0].k_cache, cases[0].block_table, S, cases[0].scale)
+    need = qf.workspace_size(desc)
+    ws = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+
+    def step(events=None):
+        for l, c in enumerate(cases):
+            if events is not None:
+                events[l][0].record()
+            qf.attn_decode_split(c.q, c.k_cache, c.v_cache, c.block_table, c.ctx_lens,
+                                 c.n_shards, max_shards=S, scale=c.scale, part_out=po,
+                                 part_lse=pl, workspace=ws)
+            if events is not None:
+                events[l][1].record()
+            qf.attn_combine(po, pl, out=out, lse=lse)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"[bench] warmup done; timing {args.steps} steps")
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(L)]
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        step(ev[k])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    ms_per_step = elapsed * 1e3 / args.steps
+    sweep_ms = [ev[k][l][0].elapsed_time(ev[k][l][1]) for k in range(args.steps) for l in range(L)]
+    sweep_avg_s = sum(sweep_ms) / len(sweep_ms) / 1e3
+    log(f"[bench] {ms_per_step:.3f} ms/step, sweep launch avg {sweep_avg_s * 1e6:.1f} us")
+
+    kv_step = sum(a["kv"] for a in ab)
+    value = kv_step / (ms_per_step / 1e3) / 1e9
+    attended = sum(a["attended"] for a in ab) / L
+    sweep_bytes = sum(a["sweep"] for a in ab) / L
+    achieved = sweep_bytes / sweep_avg_s / 1e9
+    result = {
+        "metric": "decode-attention KV GB/s (and % of HBM peak); attended tokens/s per layer",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": B, "n_q_heads": Hq, "n_kv_heads": Hkv,
+                   "head_dim": D, "page": 16, "layers": L, "max_shards": S,
+                   "context": w.ctx if w.ctx else "ragged", "kv_dtype": "bf16",
+                   "kv_bytes_per_step": kv_step, "workspace_bytes": need},
+        "hbm_peak_frac": round(value / HBM_PEAK_GBS, 4),
+        "attended_tokens_per_s_per_layer": round(attended / (ms_per_step / 1e3 / L), 1),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "kernel": "decode_split_kernel", "launch_avg_us": round(sweep_avg_s * 1e6, 2),
+                     "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] cpu_baseline: timing the fp64 oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(cases)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

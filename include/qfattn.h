@@ -1,0 +1,130 @@
+/*
+ * qfattn — split-KV grouped-query decode attention for AMD Instinct MI355X (gfx950).
+ *
+ * The operation is the cache-side sweep of the Q-First decode protocol (arXiv:2608.15473, §2):
+ * the device is given the current query of every request and returns, for each query head, the
+ * attention vector over the positions already in the KV cache together with its log-sum-exp.
+ * The cache of a request may be cut into any number of position shards; each shard returns the
+ * pair (O, ln Z) of §5,
+ *
+ *     s_i = scale * q . k_i,   Z = sum_i exp(s_i),   O = (sum_i exp(s_i) v_i) / Z,
+ *
+ * and the pairs of all shards merge into the result of one sweep over the whole cache (§5: any
+ * partition, any order; an empty shard is ln Z = -inf with a vector that is never read).
+ *
+ * Conventions shared by every entry point
+ *   - Every pointer argument except `stream` is a DEVICE pointer, owned by the caller.  The library
+ *     allocates no memory, keeps no pointer after returning and holds no per-call state.
+ *   - Every call is asynchronous: it validates its arguments on the host, enqueues its kernels on
+ *     `stream` (a hipStream_t; NULL = the legacy default stream) and returns without waiting.
+ *   - Return value: QF_OK (0) or a negative QF_E* code.  On error nothing has been enqueued, and
+ *     qf_last_error() describes the problem.  No C++ exception crosses this boundary.
+ *   - bf16 tensors are IEEE-754 binary32 truncated to the upper 16 bits (bfloat16), stored as
+ *     uint16.  All index tensors are int32.
+ *   - Device-resident contents (block-table entries, context lengths, shard counts) cannot be
+ *     checked on the host without a synchronisation.  The kernels check them instead: a value out
+ *     of range never causes an out-of-bounds access; the affected request's log-sum-exp outputs
+ *     are set to NaN so the error is visible downstream.
+ */
+#ifndef QFATTN_H
+#define QFATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define QF_VERSION 1
+
+#define QF_OK 0
+#define QF_EINVAL (-1)       /* null pointer, negative or inconsistent size, Hq % Hkv != 0   */
+#define QF_EUNSUPPORTED (-2) /* head_dim != 128, page_size != 16, Hq/Hkv not in {1,2,4,8}     */
+#define QF_EALIGN (-3)       /* a pointer is not aligned as documented below                 */
+#define QF_EHIP (-4)         /* the HIP runtime refused a launch; message from hipGetErrorString */
+
+/* Shape of one decode step.  Every field is a host value. */
+typedef struct qf_decode_desc {
+  int32_t batch;             /* B  >= 0 requests (B == 0: the calls do nothing)               */
+  int32_t n_q_heads;         /* Hq >= 1 query heads                                           */
+  int32_t n_kv_heads;        /* Hkv >= 1 KV heads; G = Hq / Hkv query heads share one KV head */
+  int32_t head_dim;          /* D, must be 128                                                */
+  int32_t page_size;         /* P, positions per cache page, must be 16                       */
+  int32_t max_pages_per_seq; /* row length (stride) of the block table, >= 1                  */
+  int32_t num_pages;         /* physical pages in the K and V pools, >= 1                     */
+  int32_t max_shards;        /* S_max >= 1, the shard-slot dimension of the partial outputs   */
+  float softmax_scale;       /* finite; logits are scale * q . k (1/sqrt(128) for Qwen3)      */
+} qf_decode_desc;
+
+/*
+ * Bytes of device workspace qf_attn_decode_split needs for this shape (0 is possible).  The
+ * workspace holds partial states of sub-shard chunks when a shape has too few (request, KV head,
+ * shard) units to fill the GPU.  Host-only; depends on the descriptor alone.
+ * Returns QF_OK, or QF_EINVAL / QF_EUNSUPPORTED for a descriptor qf_attn_decode_split rejects.
+ */
+int qf_attn_decode_split_workspace_size(const qf_decode_desc* desc, size_t* bytes);
+
+/*
+ * The sweep, split into position shards (§2 protocol, §5 shard pairs).
+ *
+ *   q           bf16 [B, Hq, D], 16-byte aligned.  Query head h reads KV head h / G.
+ *   k_cache     bf16 [num_pages, Hkv, P, D], 16-byte aligned: page p, KV head g, slot i holds the
+ *   v_cache     key (value) of the position that the block table maps to (p, i).
+ *   block_table int32 [B, max_pages_per_seq]; logical page j of request b is physical page
+ *               block_table[b * max_pages_per_seq + j].  Entries past a request's last page are
+ *               never read.  NULL means the identity map b * max_pages_per_seq + j, which needs
+ *               num_pages >= B * max_pages_per_seq.
+ *   ctx_lens    int32 [B], 0 <= n_b <= max_pages_per_seq * P: cached positions of request b
+ *               (the current token is not included, §2).
+ *   n_shards    int32 [B], 1 <= S_b <= max_shards: how many shards request b is cut into.
+ *               Shard s takes logical pages [s*K, min((s+1)*K, pages_b)) with
+ *               pages_b = ceil(n_b / P) and K = ceil(pages_b / S_b); the positions of the last
+ *               page are clipped to n_b.  Shards past the end are empty.
+ *   part_out    fp32 [B, max_shards, Hq, D], 16-byte aligned: O of shard s (normalised, §5).
+ *               Not written for empty shards or for slots s >= S_b (§5: never read).
+ *   part_lse    fp32 [B, max_shards, Hq], 4-byte aligned: natural-log ln Z of shard s; -inf for
+ *               an empty shard and for every slot s >= S_b; NaN if request b's inputs were out
+ *               of range (see above).
+ *   workspace   device buffer of at least qf_attn_decode_split_workspace_size() bytes, 16-byte
+ *               aligned; may be NULL when that size is 0.  Its contents need no initialisation
+ *               and are garbage afterwards.
+ *   stream      hipStream_t.
+ */
+int qf_attn_decode_split(const qf_decode_desc* desc, const void* q, const void* k_cache,
+                         const void* v_cache, const int32_t* block_table,
+                         const int32_t* ctx_lens, const int32_t* n_shards, float* part_out,
+                         float* part_lse, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The merge of §5 over every shard slot: for each request b and query head h,
+ *
+ *     m = max_s ln Z_s,  w_s = exp(ln Z_s - m) (w_s = 0, and O_s unread, where ln Z_s = -inf),
+ *     out = sum_s w_s O_s / sum_s w_s,   lse = m + ln(sum_s w_s),
+ *
+ * the N-way form of the pairwise lerp/sigmoid/logaddexp merge; every weight is at most 1, so
+ * nothing overflows however large the log partitions are.
+ *
+ *   part_out    fp32 [B, max_shards, Hq, D], 16-byte aligned (as written by the sweep).
+ *   part_lse    fp32 [B, max_shards, Hq], 4-byte aligned.
+ *   out         bf16 [B, Hq, D], 4-byte aligned; round-to-nearest-even.  All slots empty
+ *               (n_b = 0): +0.  A NaN log-sum-exp among the slots: NaN.
+ *   lse         fp32 [B, Hq] natural log, or NULL if not wanted.  All empty: -inf.
+ *   head_dim must be 128.
+ */
+int qf_attn_combine(int32_t batch, int32_t n_q_heads, int32_t head_dim, int32_t max_shards,
+                    const float* part_out, const float* part_lse, void* out, float* lse,
+                    void* stream);
+
+/* Message for the last error on the calling thread; "" if none.  Valid until the thread's next
+ * call into the library. */
+const char* qf_last_error(void);
+
+/* QF_VERSION of the loaded library. */
+int qf_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QFATTN_H */

@@ -1,0 +1,24 @@
+"""MI355X (gfx950) split-KV grouped-query decode attention with an LSE shard merge.
+
+The computation is the cache-side sweep of the Q-First decode protocol (arXiv:2608.15473, §2 and
+§5); it runs in hand-written HIP kernels behind the C ABI of ``include/qfattn.h``
+(``lib/libqfattn.so``).  This package is the thin Python binding over that library.
+"""
+
+from .binding import (  # noqa: F401
+    EXPORTED,
+    LIB_PATH,
+    QF_EALIGN,
+    QF_EHIP,
+    QF_EINVAL,
+    QF_EUNSUPPORTED,
+    QF_OK,
+    DecodeDesc,
+    QFError,
+    attn_combine,
+    attn_decode,
+    attn_decode_split,
+    load_library,
+    make_desc,
+    workspace_size,
+)

@@ -1,0 +1,173 @@
+"""ctypes binding of libqfattn.so (include/qfattn.h): argument marshalling only.
+
+Every step of the computation runs in the HIP kernels behind the C ABI; this module turns torch
+tensors into device pointers, picks the caller's current HIP stream and raises on error codes.
+There is no fallback: if the library is missing or the tensors are not on a GPU, calls raise.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "lib", "libqfattn.so")
+
+QF_OK, QF_EINVAL, QF_EUNSUPPORTED, QF_EALIGN, QF_EHIP = 0, -1, -2, -3, -4
+EXPORTED = ("qf_attn_decode_split_workspace_size", "qf_attn_decode_split", "qf_attn_combine",
+            "qf_last_error", "qf_version")
+
+
+class QFError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"qfattn error {code}: {msg}")
+        self.code = code
+
+
+class DecodeDesc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("max_pages_per_seq", ctypes.c_int32),
+                ("num_pages", ctypes.c_int32), ("max_shards", ctypes.c_int32),
+                ("softmax_scale", ctypes.c_float)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load (once) and return the C library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise QFError(QF_EHIP, f"{path} not found: build it with "
+                               "`python -m paper_2608_15473_amd.build`")
+    lib = ctypes.CDLL(path)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    lib.qf_attn_decode_split_workspace_size.argtypes = [ctypes.POINTER(DecodeDesc),
+                                                        ctypes.POINTER(sz)]
+    lib.qf_attn_decode_split.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp, vp, vp,
+                                         vp, vp, sz, vp]
+    lib.qf_attn_combine.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp]
+    lib.qf_last_error.restype = ctypes.c_char_p
+    lib.qf_last_error.argtypes = []
+    lib.qf_version.argtypes = []
+    for name in ("qf_attn_decode_split_workspace_size", "qf_attn_decode_split",
+                 "qf_attn_combine", "qf_version"):
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _check(rc: int) -> None:
+    if rc != QF_OK:
+        raise QFError(rc, load_library().qf_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _require(t, name, dtype, dim=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise QFError(QF_EINVAL, f"{name} must be a GPU tensor (got {t.device})")
+    if t.dtype != dtype:
+        raise QFError(QF_EINVAL, f"{name} must be {dtype} (got {t.dtype})")
+    if not t.is_contiguous():
+        raise QFError(QF_EINVAL, f"{name} must be contiguous")
+    if dim is not None and t.dim() != dim:
+        raise QFError(QF_EINVAL, f"{name} must have {dim} dimensions (got {t.dim()})")
+
+
+def make_desc(q, k_cache, block_table, max_shards, scale, num_pages=None, max_pages=None):
+    B, Hq, D = q.shape
+    P, Hkv = k_cache.shape[2], k_cache.shape[1]
+    if max_pages is None:
+        max_pages = block_table.shape[1] if block_table is not None else k_cache.shape[0] // max(B, 1)
+    return DecodeDesc(B, Hq, Hkv, D, P, int(max_pages),
+                      int(k_cache.shape[0] if num_pages is None else num_pages),
+                      int(max_shards), float(scale))
+
+
+def workspace_size(desc: DecodeDesc) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load_library().qf_attn_decode_split_workspace_size(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value
+
+
+def attn_decode_split(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards=None,
+                      scale=None, part_out=None, part_lse=None, workspace=None,
+                      max_pages=None):
+    """The sweep split into position shards (qf_attn_decode_split).
+
+    q bf16 [B, Hq, D]; k_cache / v_cache bf16 [num_pages, Hkv, P, D]; block_table int32
+    [B, max_pages] or None (identity); ctx_lens int32 [B]; n_shards an int or int32 [B].
+    Returns (part_out fp32 [B, S_max, Hq, D], part_lse fp32 [B, S_max, Hq]).
+    """
+    _require(q, "q", torch.bfloat16, 3)
+    _require(k_cache, "k_cache", torch.bfloat16, 4)
+    _require(v_cache, "v_cache", torch.bfloat16, 4)
+    if v_cache.shape != k_cache.shape:
+        raise QFError(QF_EINVAL, "k_cache and v_cache shapes differ")
+    if block_table is not None:
+        _require(block_table, "block_table", torch.int32, 2)
+    _require(ctx_lens, "ctx_lens", torch.int32, 1)
+    B = q.shape[0]
+    if isinstance(n_shards, int):
+        if max_shards is None:
+            max_shards = n_shards
+        n_shards = torch.full((B,), n_shards, dtype=torch.int32, device=q.device)
+    _require(n_shards, "n_shards", torch.int32, 1)
+    if max_shards is None:
+        raise QFError(QF_EINVAL, "max_shards is required when n_shards is a tensor")
+    if scale is None:
+        scale = q.shape[-1] ** -0.5
+    desc = make_desc(q, k_cache, block_table, max_shards, scale, max_pages=max_pages)
+    Hq, D = q.shape[1], q.shape[2]
+    if part_out is None:
+        part_out = torch.empty((B, max_shards, Hq, D), dtype=torch.float32, device=q.device)
+    if part_lse is None:
+        part_lse = torch.empty((B, max_shards, Hq), dtype=torch.float32, device=q.device)
+    _require(part_out, "part_out", torch.float32)
+    _require(part_lse, "part_lse", torch.float32)
+    need = workspace_size(desc)
+    if need and workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    stream = torch.cuda.current_stream(q.device).cuda_stream
+    _check(load_library().qf_attn_decode_split(
+        ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+        _ptr(ctx_lens), _ptr(n_shards), _ptr(part_out), _ptr(part_lse), _ptr(workspace),
+        ws_bytes, ctypes.c_void_p(stream)))
+    return part_out, part_lse
+
+
+def attn_combine(part_out, part_lse, out=None, lse=None, want_lse=True):
+    """Merge every shard slot (qf_attn_combine): returns (out bf16 [B, Hq, D], lse fp32 [B, Hq])."""
+    _require(part_out, "part_out", torch.float32, 4)
+    _require(part_lse, "part_lse", torch.float32, 3)
+    B, S, Hq, D = part_out.shape
+    if tuple(part_lse.shape) != (B, S, Hq):
+        raise QFError(QF_EINVAL, "part_lse shape does not match part_out")
+    if out is None:
+        out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=part_out.device)
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=part_out.device)
+    stream = torch.cuda.current_stream(part_out.device).cuda_stream
+    _check(load_library().qf_attn_combine(B, Hq, D, S, _ptr(part_out), _ptr(part_lse), _ptr(out),
+                                          _ptr(lse), ctypes.c_void_p(stream)))
+    return out, lse
+
+
+def attn_decode(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards=None,
+                scale=None):
+    """Sweep then merge: (out bf16 [B, Hq, D], lse fp32 [B, Hq], part_out, part_lse)."""
+    po, pl = attn_decode_split(q, k_cache, v_cache, block_table, ctx_lens, n_shards,
+                               max_shards=max_shards, scale=scale)
+    out, lse = attn_combine(po, pl)
+    return out, lse, po, pl

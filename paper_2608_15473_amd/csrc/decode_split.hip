@@ -1,0 +1,317 @@
+// Split-KV decode sweep over a paged grouped-query KV cache (gfx950).
+//
+// Computes, for every (request b, shard s, query head h), the pair (O, ln Z) of the shard's cached
+// positions (Q-First, arXiv:2608.15473, §5: Z = sum exp(s_i), O = sum exp(s_i) v_i / Z, scores
+// s_i = scale * q . k_i as in §2).  The kernel is bound by HBM bandwidth: every cached byte of K
+// and V is read exactly once, and the G query heads that share a KV head are all served from that
+// one read.
+//
+// Work decomposition.  One workgroup = one unit (b, s, c, g): KV head g of chunk c of shard s of
+// request b (chunks > 1 only when a shape has too few units to fill the GPU).  Its W wavefronts
+// take the unit's pages round-robin.  Inside a wavefront the 64 lanes form 4 rows of 16; a page
+// (16 positions x 128 dims of bf16 = 4 KB per tensor) is read with 4 fully coalesced 16-byte
+// loads per lane, load j covering positions 4j..4j+3, so lane (row r, column c) holds dims
+// 8c..8c+7 of position 4j + r.  Each row is an independent online-softmax sweeper over the
+// positions r, r+4, r+8, r+12 of every page; rows and wavefronts merge once, at the end.
+//
+// Per page and lane: QK^T with v_dot2c_f32_bf16 on the packed bf16 pairs (exact products, fp32
+// sums), a 16-lane DPP all-reduce per score, exp2 in the log2 domain, and fp32 FMAs for PV with
+// the bf16 values unpacked by shift/mask.  The running max is raised lazily (only when a score
+// exceeds it by more than kLazy), so the O rescale is rare after a shard's first pages.
+#include <math.h>
+
+#include "qf_internal.h"
+
+namespace qf {
+namespace {
+
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+
+constexpr int D = kHeadDim;
+constexpr int P = kPage;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kLazy = 8.0f;  // log2 units: p = exp2(s - m) stays <= 256 between rescales
+
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
+                                         __builtin_bit_cast(bf16x2_t, b), c, false);
+}
+
+// Sum over the 16 lanes of a DPP row; the result is bitwise identical on all 16 lanes.
+__device__ __forceinline__ float row_sum16(float x) {
+  x += __builtin_amdgcn_update_dpp(0.0f, x, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
+  x += __builtin_amdgcn_update_dpp(0.0f, x, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
+  x += __builtin_amdgcn_update_dpp(0.0f, x, 0x141, 0xF, 0xF, false);  // row_half_mirror
+  x += __builtin_amdgcn_update_dpp(0.0f, x, 0x140, 0xF, 0xF, false);  // row_mirror
+  return x;
+}
+
+// Block-table entries are wave-uniform: read them through the constant address space so they
+// become scalar loads (own counter), never vector loads that would join the page loads' vmcnt.
+typedef const __attribute__((address_space(4))) int32_t* const_i32_ptr;
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+__device__ __forceinline__ void unpack8(const uint4& w, float* f) {
+  f[0] = bf16_lo(w.x); f[1] = bf16_hi(w.x);
+  f[2] = bf16_lo(w.y); f[3] = bf16_hi(w.y);
+  f[4] = bf16_lo(w.z); f[5] = bf16_hi(w.z);
+  f[6] = bf16_lo(w.w); f[7] = bf16_hi(w.w);
+}
+
+template <int G, int W>
+__global__ void __launch_bounds__(64 * W)
+decode_split_kernel(const uint16_t* __restrict__ qp, const uint16_t* __restrict__ kp,
+                    const uint16_t* __restrict__ vp, const int32_t* __restrict__ block_table,
+                    const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ n_shards,
+                    float* __restrict__ out_o, float* __restrict__ out_lse, int32_t hq,
+                    int32_t hkv, int32_t max_pages, int32_t num_pages, int32_t max_shards,
+                    int32_t chunks, int32_t n_units, int32_t units_per_xcd, float scale_log2) {
+  // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a contiguous range of
+  // units so the KV heads of one (request, shard) share that XCD's L2 for the block table.
+  const int unit = (int)(blockIdx.x % 8u) * units_per_xcd + (int)(blockIdx.x / 8u);
+  if (unit >= n_units) return;
+  const int g = unit % hkv;
+  int rest = unit / hkv;
+  const int c = rest % chunks;
+  rest /= chunks;
+  const int s = rest % max_shards;
+  const int b = rest / max_shards;
+
+  // The request's shape, checked: an out-of-range value is clamped (so nothing is read out of
+  // bounds) and poisons this unit's log-sum-exp with NaN.
+  int n = ctx_lens[b];
+  int S = n_shards[b];
+  bool poison = false;
+  const int cap = max_pages * P;
+  if (n < 0 || n > cap) { poison = true; n = n < 0 ? 0 : cap; }
+  if (S < 1 || S > max_shards) { poison = true; S = S < 1 ? 1 : max_shards; }
+  const int pages = (n + P - 1) / P;
+  const int per = (pages + S - 1) / S;
+  int p0 = 0, p1 = 0;
+  if (s < S) {
+    p0 = (int)min((int64_t)s * per, (int64_t)pages);
+    p1 = (int)min((int64_t)(s + 1) * per, (int64_t)pages);
+  }
+  const int len = p1 - p0;
+  const int cper = (len + chunks - 1) / chunks;
+  const int c0 = p0 + (int)min((int64_t)c * cper, (int64_t)len);
+  const int c1 = p0 + (int)min((int64_t)(c + 1) * cper, (int64_t)len);
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int row = lane >> 4;
+  const int col = lane & 15;
+
+  // Queries of the group, dims 8col..8col+7, as packed bf16 pairs.
+  uint32_t qv[G][4];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    const uint4 t = reinterpret_cast<const uint4*>(qp + ((size_t)b * hq + (size_t)g * G + h) * D)[col];
+    qv[h][0] = t.x; qv[h][1] = t.y; qv[h][2] = t.z; qv[h][3] = t.w;
+  }
+
+  float m[G], l[G], acc[G][8];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    m[h] = -INFINITY;
+    l[h] = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[h][e] = 0.0f;
+  }
+
+  const const_i32_ptr bt =
+      block_table ? (const_i32_ptr)(block_table + (size_t)b * max_pages) : nullptr;
+  const size_t page_stride = (size_t)hkv * P * D;  // elements between physical pages
+  const uint16_t* kbase = kp + (size_t)g * P * D;
+  const uint16_t* vbase = vp + (size_t)g * P * D;
+
+  // This wavefront's pages: c0 + wave + i * W for i < mine.
+  const int mine = (c1 - c0 > wave) ? (c1 - c0 - wave + W - 1) / W : 0;
+  auto page_of = [&](int i) { return c0 + wave + i * W; };
+  // Raw block-table entry of page i (read two pages ahead; checked only when used, so the scalar
+  // load's latency hides behind the page in flight).
+  auto entry = [&](int i) -> int {
+    if (i >= mine) return 0;
+    const int pg = page_of(i);
+    return bt ? bt[pg] : b * max_pages + pg;
+  };
+  // One 4 KB page of one KV head through a buffer resource: a resource of size 0 (no page) turns
+  // the loads into no-ops that return zeros, so the prefetch below is unconditional and the
+  // wait counts stay static.
+  auto issue = [&](uint4* kk, uint4* vv, int ph, bool live) {
+    if ((unsigned)ph >= (unsigned)num_pages) {
+      poison |= live;
+      ph = 0;
+    }
+    const int bytes = live ? P * D * 2 : 0;
+    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(kbase + (size_t)ph * page_stride), (short)0, bytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(vbase + (size_t)ph * page_stride), (short)0, bytes, 0x00020000);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      kk[j] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, lane * 16, j * 1024, 0));
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      vv[j] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, lane * 16, j * 1024, 0));
+  };
+
+  auto process = [&](uint4* kc, uint4* vc, int pg) {
+    const int valid = n - pg * P;  // slots [0, valid) of this page are cached positions
+    if (valid < P) {
+      // Last, partial page: the slots past n hold no position.  Their values must not meet a
+      // zero weight (0 * NaN garbage = NaN), so clear them; their scores become -inf below.
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (4 * j + row >= valid) vc[j] = make_uint4(0u, 0u, 0u, 0u);
+    }
+
+    // Scores of this row's 4 positions for the G heads, log2 domain.
+    float sc[4][G];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        float d = dot2(kc[j].x, qv[h][0], 0.0f);
+        d = dot2(kc[j].y, qv[h][1], d);
+        d = dot2(kc[j].z, qv[h][2], d);
+        d = dot2(kc[j].w, qv[h][3], d);
+        d = row_sum16(d);
+        sc[j][h] = (4 * j + row < valid) ? d * scale_log2 : -INFINITY;
+      }
+    }
+
+    float pr[4][G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float mx = fmaxf(fmaxf(sc[0][h], sc[1][h]), fmaxf(sc[2][h], sc[3][h]));
+      if (mx > m[h] + kLazy) {
+        const float alpha = __builtin_amdgcn_exp2f(m[h] - mx);  // m = -inf -> 0
+        l[h] *= alpha;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[h][e] *= alpha;
+        m[h] = mx;
+      }
+      const float base = (m[h] == -INFINITY) ? 0.0f : m[h];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) pr[j][h] = __builtin_amdgcn_exp2f(sc[j][h] - base);
+      l[h] += (pr[0][h] + pr[1][h]) + (pr[2][h] + pr[3][h]);
+    }
+
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float vf[8];
+      unpack8(vc[j], vf);
+#pragma unroll
+      for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pr[j][h], vf[e], acc[h][e]);
+    }
+  };
+
+  // The query loads must have landed before the loop, so that the only loads in flight inside it
+  // are the two page buffers (vmcnt 0, expcnt 7, lgkmcnt 15).
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+
+  // Ping-pong over two register buffers: page i+1 streams in while page i is computed.
+  uint4 ka[4], va[4], kb[4], vb[4];
+  issue(ka, va, entry(0), mine > 0);
+  int ph_next = entry(1);
+  // Scalar loads may return out of order, so waiting for one waits for all: each entry is
+  // requested only after the previous one has been consumed by issue().
+  for (int i = 0; i < mine; i += 2) {
+    issue(kb, vb, ph_next, i + 1 < mine);
+    const int ph2 = entry(i + 2);
+    process(ka, va, page_of(i));
+    if (i + 1 >= mine) break;
+    issue(ka, va, ph2, i + 2 < mine);
+    ph_next = entry(i + 3);
+    process(kb, vb, page_of(i + 1));
+  }
+
+  // Merge the 4 rows of the wavefront (lanes col, col+16, col+32, col+48 hold the same dims).
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    float M = fmaxf(m[h], __shfl_xor(m[h], 16));
+    M = fmaxf(M, __shfl_xor(M, 32));
+    const float f = (M == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m[h] - M);
+    float lh = l[h] * f;
+    lh += __shfl_xor(lh, 16);
+    lh += __shfl_xor(lh, 32);
+    l[h] = lh;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float a = acc[h][e] * f;
+      a += __shfl_xor(a, 16);
+      a += __shfl_xor(a, 32);
+      acc[h][e] = a;
+    }
+    m[h] = M;
+  }
+
+  // Merge the W wavefronts through LDS and write the unit's (O, ln Z).
+  __shared__ float s_acc[W][G][D];
+  __shared__ float s_m[W][G];
+  __shared__ float s_l[W][G];
+  if (row == 0) {
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s_acc[wave][h][col * 8 + e] = acc[h][e];
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) { s_m[wave][h] = m[h]; s_l[wave][h] = l[h]; }
+  }
+  const int bad = __syncthreads_or(poison ? 1 : 0);
+
+  const size_t slot = (((size_t)b * max_shards + s) * chunks + c) * hq + (size_t)g * G;
+  for (int idx = threadIdx.x; idx < G * D; idx += 64 * W) {
+    const int h = idx / D;
+    const int d = idx % D;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < W; ++w) M = fmaxf(M, s_m[w][h]);
+    float L = 0.0f, A = 0.0f;
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < W; ++w) {
+        const float f = __builtin_amdgcn_exp2f(s_m[w][h] - M);
+        L = fmaf(f, s_l[w][h], L);
+        A = fmaf(f, s_acc[w][h][d], A);
+      }
+      out_o[(slot + h) * D + d] = A / L;
+    }
+    if (d == 0) {
+      float lse = (M == -INFINITY) ? -INFINITY : (M + log2f(L)) * kLn2;
+      if (bad) lse = NAN;
+      out_lse[slot + h] = lse;
+    }
+  }
+}
+
+template <int G>
+hipError_t launch_g(const SplitParams& p, hipStream_t stream) {
+  const unsigned grid = 8u * (unsigned)p.units_per_xcd;
+  hipLaunchKernelGGL((decode_split_kernel<G, kSplitWaves>), dim3(grid), dim3(64 * kSplitWaves),
+                     0, stream, p.q, p.k, p.v, p.block_table, p.ctx_lens, p.n_shards, p.out_o,
+                     p.out_lse, p.hq, p.hkv, p.max_pages, p.num_pages, p.max_shards, p.chunks,
+                     p.n_units, p.units_per_xcd, p.scale_log2);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_decode_split(const SplitParams& p, int group, hipStream_t stream) {
+  switch (group) {
+    case 1: return launch_g<1>(p, stream);
+    case 2: return launch_g<2>(p, stream);
+    case 4: return launch_g<4>(p, stream);
+    case 8: return launch_g<8>(p, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace qf

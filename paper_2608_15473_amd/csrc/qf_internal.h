@@ -1,0 +1,47 @@
+// Internal interface between the host library (qfattn_api.hip) and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace qf {
+
+constexpr int kHeadDim = 128;     // D
+constexpr int kPage = 16;         // P
+constexpr int kSplitWaves = 4;    // waves per workgroup of the sweep kernel
+constexpr int kMergeWaves = 4;    // waves per workgroup of the merge kernel
+
+// One launch of the sweep kernel.  A workgroup handles one unit (request b, shard s, chunk c,
+// KV head g); its output slot is [((b * max_shards + s) * chunks + c) * hq + g * G + h].
+struct SplitParams {
+  const uint16_t* q;            // bf16 [B, Hq, D]
+  const uint16_t* k;            // bf16 [num_pages, Hkv, P, D]
+  const uint16_t* v;
+  const int32_t* block_table;   // [B, max_pages] or null (identity)
+  const int32_t* ctx_lens;      // [B]
+  const int32_t* n_shards;      // [B]
+  float* out_o;                 // fp32 [B, max_shards, chunks, Hq, D]
+  float* out_lse;               // fp32 [B, max_shards, chunks, Hq]
+  int32_t batch, hq, hkv, max_pages, num_pages, max_shards, chunks;
+  int32_t n_units;              // B * max_shards * chunks * Hkv
+  int32_t units_per_xcd;        // ceil(n_units / 8)
+  float scale_log2;             // softmax scale * log2(e)
+};
+
+// Merge of `entries` partial states per (row, head):
+//   in  O [rows, entries, hq, D] fp32, lse [rows, entries, hq] fp32 (natural log)
+//   out O [rows, hq, D] (fp32 or bf16), lse [rows, hq] fp32 (may be null)
+struct MergeParams {
+  const float* in_o;
+  const float* in_lse;
+  void* out_o;
+  float* out_lse;
+  int32_t rows, entries, hq;
+};
+
+hipError_t launch_decode_split(const SplitParams& p, int group, hipStream_t stream);
+// to_bf16 = false: partial-state output (fp32 O not written for an empty row);
+// to_bf16 = true:  final output (bf16, +0 for an empty row).
+hipError_t launch_merge(const MergeParams& p, bool to_bf16, hipStream_t stream);
+
+}  // namespace qf

@@ -1,0 +1,190 @@
+// Host side of the C-ABI: argument validation, the chunking rule, launches on the caller's stream.
+// Declarations and the full contract are in include/qfattn.h.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "qf_internal.h"
+#include "qfattn.h"
+
+namespace {
+
+thread_local char g_error[512];
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_error, sizeof g_error, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// Target number of sweep workgroups: 8 per compute unit of an MI355X (256 CUs).  Depends on the
+// descriptor only, so a given shape always runs the same decomposition (and gives the same bits).
+constexpr int64_t kTargetWorkgroups = 2048;
+constexpr int64_t kMinPagesPerWave = 2;
+
+int check_desc(const qf_decode_desc* d) {
+  if (!d) return fail(QF_EINVAL, "desc is NULL");
+  if (d->batch < 0) return fail(QF_EINVAL, "batch %d < 0", d->batch);
+  if (d->n_q_heads < 1 || d->n_kv_heads < 1)
+    return fail(QF_EINVAL, "n_q_heads %d / n_kv_heads %d must be >= 1", d->n_q_heads, d->n_kv_heads);
+  if (d->n_q_heads % d->n_kv_heads != 0)
+    return fail(QF_EINVAL, "n_q_heads %d is not a multiple of n_kv_heads %d", d->n_q_heads,
+                d->n_kv_heads);
+  const int G = d->n_q_heads / d->n_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(QF_EUNSUPPORTED, "group size %d (n_q_heads / n_kv_heads) not in {1,2,4,8}", G);
+  if (d->head_dim != qf::kHeadDim)
+    return fail(QF_EUNSUPPORTED, "head_dim %d != %d", d->head_dim, qf::kHeadDim);
+  if (d->page_size != qf::kPage)
+    return fail(QF_EUNSUPPORTED, "page_size %d != %d", d->page_size, qf::kPage);
+  if (d->max_pages_per_seq < 1) return fail(QF_EINVAL, "max_pages_per_seq %d < 1", d->max_pages_per_seq);
+  if ((int64_t)d->max_pages_per_seq * qf::kPage > INT32_MAX)
+    return fail(QF_EINVAL, "max_pages_per_seq %d too large", d->max_pages_per_seq);
+  if (d->num_pages < 1) return fail(QF_EINVAL, "num_pages %d < 1", d->num_pages);
+  if (d->max_shards < 1) return fail(QF_EINVAL, "max_shards %d < 1", d->max_shards);
+  if (!isfinite(d->softmax_scale)) return fail(QF_EINVAL, "softmax_scale is not finite");
+  return QF_OK;
+}
+
+int64_t choose_chunks(const qf_decode_desc* d) {
+  const int64_t units = (int64_t)d->batch * d->n_kv_heads * d->max_shards;
+  if (units <= 0) return 1;
+  const int64_t est_pages = (d->max_pages_per_seq + d->max_shards - 1) / d->max_shards;
+  int64_t c = (kTargetWorkgroups + units - 1) / units;
+  c = std::min(c, std::max<int64_t>(1, est_pages / (qf::kSplitWaves * kMinPagesPerWave)));
+  return std::max<int64_t>(1, std::min<int64_t>(c, 1024));
+}
+
+size_t workspace_bytes(const qf_decode_desc* d, int64_t chunks) {
+  if (chunks <= 1) return 0;
+  const size_t states = (size_t)d->batch * d->max_shards * chunks * d->n_q_heads;
+  return states * qf::kHeadDim * sizeof(float) + states * sizeof(float);
+}
+
+}  // namespace
+
+extern "C" {
+
+int qf_version(void) { return QF_VERSION; }
+
+const char* qf_last_error(void) { return g_error; }
+
+int qf_attn_decode_split_workspace_size(const qf_decode_desc* desc, size_t* bytes) {
+  g_error[0] = 0;
+  const int rc = check_desc(desc);
+  if (rc) return rc;
+  if (!bytes) return fail(QF_EINVAL, "bytes is NULL");
+  *bytes = workspace_bytes(desc, choose_chunks(desc));
+  return QF_OK;
+}
+
+int qf_attn_decode_split(const qf_decode_desc* desc, const void* q, const void* k_cache,
+                         const void* v_cache, const int32_t* block_table,
+                         const int32_t* ctx_lens, const int32_t* n_shards, float* part_out,
+                         float* part_lse, void* workspace, size_t workspace_size, void* stream) {
+  g_error[0] = 0;
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  const qf_decode_desc& d = *desc;
+  if (d.batch == 0) return QF_OK;
+  if (!q || !k_cache || !v_cache || !ctx_lens || !n_shards || !part_out || !part_lse)
+    return fail(QF_EINVAL, "a required pointer is NULL");
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(part_out, 16))
+    return fail(QF_EALIGN, "q, k_cache, v_cache and part_out must be 16-byte aligned");
+  if (!aligned(part_lse, 4) || !aligned(ctx_lens, 4) || !aligned(n_shards, 4) ||
+      (block_table && !aligned(block_table, 4)))
+    return fail(QF_EALIGN, "part_lse, ctx_lens, n_shards and block_table must be 4-byte aligned");
+  if (!block_table && (int64_t)d.batch * d.max_pages_per_seq > d.num_pages)
+    return fail(QF_EINVAL, "identity block table needs num_pages >= batch * max_pages_per_seq (%lld > %d)",
+                (long long)d.batch * d.max_pages_per_seq, d.num_pages);
+
+  const int64_t chunks = choose_chunks(&d);
+  const size_t need = workspace_bytes(&d, chunks);
+  if (need) {
+    if (!workspace) return fail(QF_EINVAL, "this shape needs %zu bytes of workspace", need);
+    if (workspace_size < need)
+      return fail(QF_EINVAL, "workspace of %zu bytes < %zu needed", workspace_size, need);
+    if (!aligned(workspace, 16)) return fail(QF_EALIGN, "workspace must be 16-byte aligned");
+  }
+  const int64_t units = (int64_t)d.batch * d.max_shards * chunks * d.n_kv_heads;
+  if (units > (int64_t)INT32_MAX - 8) return fail(QF_EINVAL, "too many work units (%lld)", (long long)units);
+
+  qf::SplitParams p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(k_cache);
+  p.v = static_cast<const uint16_t*>(v_cache);
+  p.block_table = block_table;
+  p.ctx_lens = ctx_lens;
+  p.n_shards = n_shards;
+  const size_t states = (size_t)d.batch * d.max_shards * chunks * d.n_q_heads;
+  if (chunks > 1) {
+    p.out_o = static_cast<float*>(workspace);
+    p.out_lse = static_cast<float*>(workspace) + states * qf::kHeadDim;
+  } else {
+    p.out_o = part_out;
+    p.out_lse = part_lse;
+  }
+  p.batch = d.batch;
+  p.hq = d.n_q_heads;
+  p.hkv = d.n_kv_heads;
+  p.max_pages = d.max_pages_per_seq;
+  p.num_pages = d.num_pages;
+  p.max_shards = d.max_shards;
+  p.chunks = (int32_t)chunks;
+  p.n_units = (int32_t)units;
+  p.units_per_xcd = (int32_t)((units + 7) / 8);
+  p.scale_log2 = (float)((double)d.softmax_scale * 1.4426950408889634);
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = qf::launch_decode_split(p, d.n_q_heads / d.n_kv_heads, s);
+  if (e != hipSuccess) return fail(QF_EHIP, "decode_split launch: %s", hipGetErrorString(e));
+  if (chunks > 1) {
+    qf::MergeParams m{};
+    m.in_o = p.out_o;
+    m.in_lse = p.out_lse;
+    m.out_o = part_out;
+    m.out_lse = part_lse;
+    m.rows = d.batch * d.max_shards;
+    m.entries = (int32_t)chunks;
+    m.hq = d.n_q_heads;
+    e = qf::launch_merge(m, false, s);
+    if (e != hipSuccess) return fail(QF_EHIP, "chunk merge launch: %s", hipGetErrorString(e));
+  }
+  return QF_OK;
+}
+
+int qf_attn_combine(int32_t batch, int32_t n_q_heads, int32_t head_dim, int32_t max_shards,
+                    const float* part_out, const float* part_lse, void* out, float* lse,
+                    void* stream) {
+  g_error[0] = 0;
+  if (batch < 0) return fail(QF_EINVAL, "batch %d < 0", batch);
+  if (n_q_heads < 1) return fail(QF_EINVAL, "n_q_heads %d < 1", n_q_heads);
+  if (max_shards < 1) return fail(QF_EINVAL, "max_shards %d < 1", max_shards);
+  if (head_dim != qf::kHeadDim) return fail(QF_EUNSUPPORTED, "head_dim %d != %d", head_dim, qf::kHeadDim);
+  if (batch == 0) return QF_OK;
+  if (!part_out || !part_lse || !out) return fail(QF_EINVAL, "a required pointer is NULL");
+  if (!aligned(part_out, 16)) return fail(QF_EALIGN, "part_out must be 16-byte aligned");
+  if (!aligned(part_lse, 4) || !aligned(out, 4) || (lse && !aligned(lse, 4)))
+    return fail(QF_EALIGN, "part_lse, out and lse must be 4-byte aligned");
+  if ((int64_t)batch * n_q_heads > INT32_MAX) return fail(QF_EINVAL, "batch * n_q_heads too large");
+  qf::MergeParams m{};
+  m.in_o = part_out;
+  m.in_lse = part_lse;
+  m.out_o = out;
+  m.out_lse = lse;
+  m.rows = batch;
+  m.entries = max_shards;
+  m.hq = n_q_heads;
+  const hipError_t e = qf::launch_merge(m, true, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(QF_EHIP, "combine launch: %s", hipGetErrorString(e));
+  return QF_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,139 @@
+"""The C ABI without a GPU: the library loads, exports what include/qfattn.h declares, and rejects
+bad arguments on the host with the documented codes before anything is launched."""
+
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2608_15473_amd as qf
+from paper_2608_15473_amd.binding import DecodeDesc, load_library
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qfattn.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(qf.LIB_PATH),
+                                reason="libqfattn.so not built (python -m paper_2608_15473_amd.build)")
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(qf_\w+)\s*\(", text, re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    lib = load_library()
+    names = _declared()
+    assert set(names) == set(qf.EXPORTED)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_version_and_error_codes_match_header():
+    text = open(HEADER).read()
+    assert load_library().qf_version() == int(re.search(r"#define QF_VERSION (\d+)", text).group(1))
+    for name, val in [("QF_OK", qf.QF_OK), ("QF_EINVAL", qf.QF_EINVAL),
+                      ("QF_EUNSUPPORTED", qf.QF_EUNSUPPORTED), ("QF_EALIGN", qf.QF_EALIGN),
+                      ("QF_EHIP", qf.QF_EHIP)]:
+        m = re.search(rf"#define {name} \(?(-?\d+)\)?", text)
+        assert int(m.group(1)) == val
+
+
+def _desc(**kw):
+    base = dict(batch=2, n_q_heads=16, n_kv_heads=8, head_dim=128, page_size=16,
+                max_pages_per_seq=64, num_pages=128, max_shards=4,
+                softmax_scale=1 / math.sqrt(128))
+    base.update(kw)
+    return DecodeDesc(**base)
+
+
+def _ws(desc):
+    n = ctypes.c_size_t(0)
+    rc = load_library().qf_attn_decode_split_workspace_size(ctypes.byref(desc), ctypes.byref(n))
+    return rc, n.value
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(batch=-1), qf.QF_EINVAL),
+    (dict(n_q_heads=0), qf.QF_EINVAL),
+    (dict(n_q_heads=12, n_kv_heads=8), qf.QF_EINVAL),
+    (dict(n_q_heads=48, n_kv_heads=3), qf.QF_EUNSUPPORTED),
+    (dict(n_q_heads=32, n_kv_heads=2), qf.QF_EUNSUPPORTED),
+    (dict(head_dim=64), qf.QF_EUNSUPPORTED),
+    (dict(page_size=32), qf.QF_EUNSUPPORTED),
+    (dict(max_pages_per_seq=0), qf.QF_EINVAL),
+    (dict(num_pages=0), qf.QF_EINVAL),
+    (dict(max_shards=0), qf.QF_EINVAL),
+    (dict(softmax_scale=float("nan")), qf.QF_EINVAL),
+    (dict(max_pages_per_seq=1 << 28), qf.QF_EINVAL),
+])
+def test_bad_descriptor_is_rejected(kw, code):
+    rc, _ = _ws(_desc(**kw))
+    assert rc == code
+    assert load_library().qf_last_error().decode() != ""
+    # the sweep entry point rejects the same descriptor before any launch
+    lib = load_library()
+    d = _desc(**kw)
+    p = ctypes.c_void_p(16)
+    rc2 = lib.qf_attn_decode_split(ctypes.byref(d), p, p, p, p, p, p, p, p, p, 1 << 30, None)
+    assert rc2 == code
+
+
+def test_workspace_only_when_units_are_few():
+    rc, n = _ws(_desc(batch=32, max_shards=64, max_pages_per_seq=2048, num_pages=65536))
+    assert rc == 0 and n == 0
+    rc, n = _ws(_desc(batch=1, max_shards=16, max_pages_per_seq=65536, num_pages=65536))
+    assert rc == 0 and n > 0
+    assert n % 16 == 0
+
+
+def test_null_and_misaligned_pointers_are_rejected_before_launch():
+    lib = load_library()
+    d = _desc()
+    a = ctypes.c_void_p(4096)
+    odd = ctypes.c_void_p(4096 + 8)
+    args = [a, a, a, a, a, a, a, a]
+    rc = lib.qf_attn_decode_split(ctypes.byref(d), None, *args[1:], None, 0, None)
+    assert rc == qf.QF_EINVAL
+    rc = lib.qf_attn_decode_split(ctypes.byref(d), odd, a, a, a, a, a, a, a, None, 0, None)
+    assert rc == qf.QF_EALIGN
+    rc = lib.qf_attn_decode_split(ctypes.byref(d), a, a, a, a, a, a, a, ctypes.c_void_p(4098),
+                                  None, 0, None)
+    assert rc == qf.QF_EALIGN
+    # identity table with too small a pool
+    rc = lib.qf_attn_decode_split(ctypes.byref(_desc(num_pages=100)), a, a, a, None, a, a, a, a,
+                                  None, 0, None)
+    assert rc == qf.QF_EINVAL
+    # a shape that needs workspace, called without one
+    d1 = _desc(batch=1, max_shards=16, max_pages_per_seq=65536, num_pages=65536)
+    rc = lib.qf_attn_decode_split(ctypes.byref(d1), a, a, a, a, a, a, a, a, None, 0, None)
+    assert rc == qf.QF_EINVAL and "workspace" in lib.qf_last_error().decode()
+
+
+def test_combine_rejects_bad_arguments():
+    lib = load_library()
+    a = ctypes.c_void_p(4096)
+    assert lib.qf_attn_combine(-1, 16, 128, 4, a, a, a, a, None) == qf.QF_EINVAL
+    assert lib.qf_attn_combine(2, 0, 128, 4, a, a, a, a, None) == qf.QF_EINVAL
+    assert lib.qf_attn_combine(2, 16, 64, 4, a, a, a, a, None) == qf.QF_EUNSUPPORTED
+    assert lib.qf_attn_combine(2, 16, 128, 0, a, a, a, a, None) == qf.QF_EINVAL
+    assert lib.qf_attn_combine(2, 16, 128, 4, None, a, a, a, None) == qf.QF_EINVAL
+    assert lib.qf_attn_combine(2, 16, 128, 4, ctypes.c_void_p(4104), a, a, a, None) == qf.QF_EALIGN
+    assert lib.qf_attn_combine(0, 16, 128, 4, None, None, None, None, None) == qf.QF_OK
+
+
+def test_empty_batch_is_a_no_op():
+    lib = load_library()
+    d = _desc(batch=0)
+    assert lib.qf_attn_decode_split(ctypes.byref(d), None, None, None, None, None, None, None,
+                                    None, None, 0, None) == qf.QF_OK
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    q = torch.zeros(1, 16, 128, dtype=torch.bfloat16)
+    k = torch.zeros(4, 8, 16, 128, dtype=torch.bfloat16)
+    with pytest.raises(qf.QFError):
+        qf.attn_decode_split(q, k, k, None, torch.zeros(1, dtype=torch.int32), 1)

@@ -1,0 +1,190 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle on the same seeded bytes.
+
+Small cases run the oracle on every output; they span several pages per wavefront, ragged last
+pages, empty shards and requests, every supported group size, the identity and permuted block
+tables and the chunked (sub-shard) path.  Full-size cases run each registered workload's layer at
+its real shape, in the launch configuration the bench times, and check sampled (request, head)
+outputs one by one.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_15473_amd as qf
+from parity import check, oracle_ref, run_gpu, say
+from workloads import WORKLOADS, make_case, workload_case
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(case, label, pairs=None):
+    say(f"[parity] {label}: B,Hq,Hkv,D={case.shape} ctx={case.ctx_lens.tolist()[:8]} "
+        f"S={case.n_shards.tolist()[:8]} S_max={case.max_shards}")
+    got = run_gpu(case)
+    ref = oracle_ref(case, pairs)
+    worst = check(case, got, ref, pairs, label)
+    say(f"[parity] {label}: ok {worst}")
+    return got, ref
+
+
+@pytest.mark.parametrize("G", [1, 2, 4, 8])
+def test_group_sizes_ragged(gpu, G):
+    case = make_case(3, 2 * G, 2, [1000, 37, 517], [5, 2, 3], seed=100 + G, device=gpu)
+    _run(case, f"G={G} ragged")
+
+
+def test_empty_requests_and_more_shards_than_pages(gpu):
+    case = make_case(4, 16, 8, [0, 16, 33, 100], [3, 4, 7, 1], seed=110, max_shards=8,
+                     device=gpu)
+    got, _ = _run(case, "empty/short")
+    assert np.all(got["part_lse"][0] == -np.inf)
+    assert np.all(got["out_bits"][0] == 0) and np.all(got["lse"][0] == -np.inf)
+    # slots past S_b are -inf even though the buffers were NaN-poisoned before the call
+    assert np.all(got["part_lse"][3, 1:] == -np.inf)
+
+
+def test_identity_table(gpu):
+    case = make_case(2, 16, 8, [700, 300], [3, 2], seed=120, table="identity", device=gpu)
+    got = run_gpu(case)
+    case_null = make_case(2, 16, 8, [700, 300], [3, 2], seed=120, table="identity", device=gpu)
+    case_null.block_table = None
+    got_null = run_gpu(case_null)
+    for key in ("part_lse", "out_bits", "lse"):
+        assert np.array_equal(got[key], got_null[key], equal_nan=True)
+    ref = oracle_ref(case)
+    check(case, got, ref, label="identity")
+
+
+def test_chunked_path(gpu):
+    """Few (request, KV head, shard) units and long shards: the sweep splits every shard into
+    chunks and merges them before returning the per-shard pairs."""
+    case = make_case(1, 8, 2, [20011], [3], seed=130, max_shards=3, device=gpu)
+    desc = qf.make_desc(case.q, case.k_cache, case.block_table, case.max_shards, case.scale)
+    assert qf.workspace_size(desc) > 0
+    _run(case, "chunked")
+
+
+def test_physical_page_placement_is_bitwise_irrelevant(gpu):
+    """The same logical cache stored contiguously or scattered over a permuted pool gives
+    bitwise identical results."""
+    a = make_case(2, 16, 8, [900, 555], [4, 3], seed=140, table="identity", device=gpu)
+    b = make_case(2, 16, 8, [900, 555], [4, 3], seed=141, device=gpu)
+    # move a's logical pages to b's physical placement
+    bt = b.block_table.long()
+    P = a.k_cache.shape[0] // 2
+    k = torch.zeros_like(b.k_cache)
+    v = torch.zeros_like(b.v_cache)
+    for r in range(2):
+        n_pg = -(-int(a.ctx_lens[r]) // 16)
+        k[bt[r, :n_pg]] = a.k_cache[r * P: r * P + n_pg]
+        v[bt[r, :n_pg]] = a.v_cache[r * P: r * P + n_pg]
+    b.k_cache, b.v_cache, b.q = k, v, a.q
+    ga, gb = run_gpu(a), run_gpu(b)
+    for key in ("part_out", "part_lse", "out_bits", "lse"):
+        assert np.array_equal(ga[key], gb[key], equal_nan=True), key
+
+
+def test_repeat_calls_are_deterministic(gpu):
+    case = make_case(2, 32, 8, [3000, 1234], [6, 2], seed=150, device=gpu)
+    g1, g2 = run_gpu(case), run_gpu(case)
+    for key in ("part_out", "part_lse", "out_bits", "lse"):
+        assert np.array_equal(g1[key], g2[key], equal_nan=True), key
+
+
+def test_planted_large_logits_stay_finite(gpu):
+    """Logits near 85 over many positions: ln Z ~ 91 > ln(FLT_MAX), where a naive fp32 sum of
+    exponentials overflows; every output must stay finite and match the oracle."""
+    case = make_case(1, 16, 8, [30000], [4], seed=160, planted=(400, 84.0, 86.0), device=gpu)
+    got, ref = _run(case, "planted ~85")
+    assert np.all(np.isfinite(got["out"])) and np.all(np.isfinite(got["lse"]))
+    assert np.all(ref["lse"] > 88.8)
+
+
+def test_planted_secondary_reading(gpu):
+    """The paper's number read the other way: ln Z ~ 85 with logits near 79."""
+    case = make_case(1, 16, 8, [30000], [4], seed=161, planted=(400, 78.0, 80.0), device=gpu)
+    got, ref = _run(case, "planted ~79")
+    assert np.all(np.abs(ref["lse"] - 85.0) < 1.5)
+
+
+def test_out_of_range_device_values_poison_lse(gpu):
+    """Out-of-range context length, shard count or block-table entry: the kernel clamps (no
+    out-of-bounds access) and the affected request's lse becomes NaN; other requests are exact."""
+    case = make_case(3, 16, 8, [500, 500, 500], [2, 2, 2], seed=170, device=gpu)
+    case.block_table[1, 3] = case.k_cache.shape[0] + 5        # entry past the pool
+    case.ctx_lens[2] = 10**6                                  # longer than the table row
+    got = run_gpu(case)
+    assert np.all(np.isnan(got["lse"][1])) and np.all(np.isnan(got["lse"][2]))
+    assert np.all(np.isnan(got["out"][1])) and np.all(np.isnan(got["out"][2]))
+    ok = make_case(3, 16, 8, [500, 500, 500], [2, 2, 2], seed=170, device=gpu)
+    ref = oracle_ref(ok, pairs=[(0, h) for h in range(16)])
+    check(ok, got, ref, pairs=[(0, h) for h in range(16)], label="poison/request0")
+    bad_s = make_case(2, 16, 8, [300, 300], [2, 99], seed=171, max_shards=4, device=gpu)
+    g2 = run_gpu(bad_s)
+    assert np.all(np.isnan(g2["lse"][1])) and np.all(np.isfinite(g2["lse"][0]))
+
+
+def test_empty_batch(gpu):
+    q = torch.zeros(0, 16, 128, dtype=torch.bfloat16, device=gpu)
+    k = torch.zeros(1, 8, 16, 128, dtype=torch.bfloat16, device=gpu)
+    po, pl = qf.attn_decode_split(q, k, k, None, torch.zeros(0, dtype=torch.int32, device=gpu), 1)
+    out, lse = qf.attn_combine(po, pl)
+    torch.cuda.synchronize()
+    assert out.shape == (0, 16, 128)
+
+
+def test_combine_selects_empty_slots_and_propagates_nan(gpu):
+    B, S, Hq, D = 2, 6, 4, 128
+    rng = np.random.default_rng(3)
+    po = rng.standard_normal((B, S, Hq, D)).astype(np.float32)
+    pl = (rng.standard_normal((B, S, Hq)) * 30 + 50).astype(np.float32)
+    pl[0, 2:] = -np.inf
+    po[0, 2:] = np.nan                        # garbage behind -inf: never read
+    pl[1, :, 0] = -np.inf                     # a fully empty (request, head)
+    pl[1, 3, 1] = np.nan                      # a NaN log partition poisons its head
+    pl[1, :, 2] = [900.0, 899.0, -np.inf, 100.0, 901.0, -800.0]   # far beyond exp's range
+    out, lse = qf.attn_combine(torch.from_numpy(po).to(gpu), torch.from_numpy(pl).to(gpu))
+    torch.cuda.synchronize()
+    out, lse = out.float().cpu().numpy(), lse.cpu().numpy()
+    import oracle
+    ro, rl = oracle.combine_max_shifted(np.where(np.isnan(po), 0, po).astype(np.float64),
+                                        np.where(np.isnan(pl), -np.inf, pl).astype(np.float64))
+    fo, fl = oracle.fold_combine(po.astype(np.float64), pl.astype(np.float64),
+                                 rng=np.random.default_rng(0))
+    for b, h in [(0, 0), (0, 1), (0, 3), (1, 2), (1, 3)]:
+        assert abs(lse[b, h] - rl[b, h]) <= 1e-5 * max(1, abs(rl[b, h]))
+        np.testing.assert_allclose(out[b, h], fo[b, h], rtol=8e-3, atol=1e-6)
+        assert abs(fl[b, h] - rl[b, h]) < 1e-9 * max(1, abs(rl[b, h]))
+    assert np.all(out[1, 0] == 0) and lse[1, 0] == -np.inf
+    assert np.all(np.isnan(out[1, 1])) and np.isnan(lse[1, 1])
+
+
+# ------------------------------------------------------------------------------------------------
+# full-size workloads: one layer at its real shape, sampled outputs
+# ------------------------------------------------------------------------------------------------
+_SAMPLES = {
+    "qwen3-0.6b_b1_n4608_s8": None,                                   # every output
+    "qwen3-0.6b_b32_n32768_s64_l28": [(0, 0), (7, 5), (19, 11), (31, 15)],
+    "qwen3-4b_b16_n36480_s32_l36": [(0, 0), (5, 13), (15, 31)],
+    "qwen3-0.6b_b1_n1m_s16_l28_planted": [(0, 0), (0, 9)],
+    "qwen3-4b_ragged_b64": "ragged",
+}
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", list(_SAMPLES))
+def test_full_size_workload_layer(gpu, name):
+    layer = 1 if WORKLOADS[name].layers > 1 else 0
+    case = workload_case(name, layer=layer, device=gpu)
+    pairs = _SAMPLES[name]
+    if pairs == "ragged":
+        n = case.ctx_lens.cpu().numpy()
+        order = np.argsort(n)
+        pairs = [(int(order[0]), 3), (int(order[32]), 17), (int(order[-1]), 30)]
+    got, ref = _run(case, f"{name} layer {layer}", pairs)
+    if name.endswith("planted"):
+        assert np.all(np.isfinite(got["out"])) and np.all(np.isfinite(got["lse"]))
+        assert np.all(got["lse"] > 88.0)
+    del case
+    torch.cuda.empty_cache()
