@@ -52,7 +52,7 @@ def algorithmic_bytes(case):
 
 def cpu_baseline(cases, budget_s=15.0):
     """The fp64 oracle (sweep per shard + pairwise merge) timed on the host over a bounded sample:
-    whole requests of the first layer, added until about ``budget_s`` of CPU work.  Device-to-host
+    whole requests, layer after layer, added until about ``budget_s`` of CPU work.  Device-to-host
     copies are excluded from the timing."""
     import numpy as np
     import torch
@@ -60,33 +60,36 @@ def cpu_baseline(cases, budget_s=15.0):
 
     import oracle
 
-    case = cases[0]
-    B, Hq, Hkv, D = case.shape
-    ctx = case.ctx_lens.cpu().numpy()
-    S = case.n_shards.cpu().numpy()
-    bt = case.block_table.cpu().numpy()
-    q = case.q.double().cpu().numpy()
-    done_bytes, spent, reqs = 0, 0.0, 0
-    order = np.argsort(ctx)[::-1] if len(ctx) > 1 else [0]
-    for b in order:
-        npg = -(-int(ctx[b]) // 16)
-        idx = torch.as_tensor(bt[b, :npg], dtype=torch.long, device=case.k_cache.device)
-        k = case.k_cache.index_select(0, idx).float().cpu().numpy()
-        v = case.v_cache.index_select(0, idx).float().cpu().numpy()
-        table = np.arange(npg)[None, :]
-        t0 = time.perf_counter()
-        po, pl = oracle.decode_split(q[b:b + 1], k, v, table, ctx[b:b + 1], S[b:b + 1],
-                                     case.scale, int(S[b]))
-        oracle.fold_combine(po, pl)
-        spent += time.perf_counter() - t0
-        done_bytes += int(ctx[b]) * 2 * Hkv * D * 2
-        reqs += 1
+    B, Hq, Hkv, D = cases[0].shape
+    done_bytes, spent, reqs, layers = 0, 0.0, 0, 0
+    for case in cases:
+        layers += 1
+        ctx = case.ctx_lens.cpu().numpy()
+        S = case.n_shards.cpu().numpy()
+        bt = case.block_table.cpu().numpy()
+        q = case.q.double().cpu().numpy()
+        for b in np.argsort(ctx)[::-1]:
+            npg = -(-int(ctx[b]) // 16)
+            idx = torch.as_tensor(bt[b, :npg], dtype=torch.long, device=case.k_cache.device)
+            k = case.k_cache.index_select(0, idx).float().cpu().numpy()
+            v = case.v_cache.index_select(0, idx).float().cpu().numpy()
+            table = np.arange(npg)[None, :]
+            t0 = time.perf_counter()
+            po, pl = oracle.decode_split(q[b:b + 1], k, v, table, ctx[b:b + 1], S[b:b + 1],
+                                         case.scale, int(S[b]))
+            oracle.fold_combine(po, pl)
+            spent += time.perf_counter() - t0
+            done_bytes += int(ctx[b]) * 2 * Hkv * D * 2
+            reqs += 1
+            if spent >= budget_s:
+                break
         if spent >= budget_s:
             break
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     return {"value": done_bytes / spent / 1e9, "unit": "GB/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"{reqs} whole request(s) of layer 0 ({done_bytes / 1e6:.0f} MB of KV, all "
+            "sample": f"{reqs} whole request(s) from the first {layers} layer(s) "
+                      f"({done_bytes / 1e6:.0f} MB of KV, all "
                       f"{Hq} heads, per-shard partials + pairwise merge), {spent:.1f} s; host has "
                       f"{len(os.sched_getaffinity(0))} usable cores"}
 
@@ -100,6 +103,9 @@ def main():
     ap.add_argument("--layers", type=int, default=None,
                     help="resident layers (default: the workload's own count)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="instead of the bench: one plain device copy of this many MiB (the "
+                         "known-size reference that scales the FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -116,6 +122,14 @@ def main():
         sys.exit(2)
     qf.load_library()
     dev = torch.device("cuda:0")
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib << 20
+        src = torch.ones(n // 4, dtype=torch.int32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n, "read_bytes": n, "write_bytes": n}))
+        return
     w = WORKLOADS[args.workload]
     L = args.layers or w.layers
     log(f"[bench] generating {L} layer(s) of {w.name} on {torch.cuda.get_device_name(0)}")

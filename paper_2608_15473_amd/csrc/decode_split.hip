@@ -30,6 +30,7 @@ typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
 constexpr int D = kHeadDim;
 constexpr int P = kPage;
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr int kNonTemporal = 2;  // buffer-load cache-policy bit "nt" on gfx950
 constexpr float kLazy = 8.0f;  // log2 units: p = exp2(s - m) stays <= 256 between rescales
 
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
@@ -60,7 +61,7 @@ __device__ __forceinline__ void unpack8(const uint4& w, float* f) {
   f[6] = bf16_lo(w.w); f[7] = bf16_hi(w.w);
 }
 
-template <int G, int W>
+template <int G, int W, int NBUF>
 __global__ void __launch_bounds__(64 * W)
 decode_split_kernel(const uint16_t* __restrict__ qp, const uint16_t* __restrict__ kp,
                     const uint16_t* __restrict__ vp, const int32_t* __restrict__ block_table,
@@ -139,7 +140,9 @@ decode_split_kernel(const uint16_t* __restrict__ qp, const uint16_t* __restrict_
   };
   // One 4 KB page of one KV head through a buffer resource: a resource of size 0 (no page) turns
   // the loads into no-ops that return zeros, so the prefetch below is unconditional and the
-  // wait counts stay static.
+  // wait counts stay static.  The loads are non-temporal (cache policy nt): every cached byte
+  // is read exactly once per sweep, and on gfx950 streaming reads marked nt reach a markedly
+  // higher share of HBM bandwidth than default-policy reads.
   auto issue = [&](uint4* kk, uint4* vv, int ph, bool live) {
     if ((unsigned)ph >= (unsigned)num_pages) {
       poison |= live;
@@ -152,10 +155,10 @@ decode_split_kernel(const uint16_t* __restrict__ qp, const uint16_t* __restrict_
         const_cast<uint16_t*>(vbase + (size_t)ph * page_stride), (short)0, bytes, 0x00020000);
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      kk[j] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, lane * 16, j * 1024, 0));
+      kk[j] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, lane * 16, j * 1024, kNonTemporal));
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      vv[j] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, lane * 16, j * 1024, 0));
+      vv[j] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, lane * 16, j * 1024, kNonTemporal));
   };
 
   auto process = [&](uint4* kc, uint4* vc, int pg) {
@@ -215,21 +218,24 @@ decode_split_kernel(const uint16_t* __restrict__ qp, const uint16_t* __restrict_
   // are the two page buffers (vmcnt 0, expcnt 7, lgkmcnt 15).
   __builtin_amdgcn_s_waitcnt(0x0F70);
 
-  // Ping-pong over two register buffers: page i+1 streams in while page i is computed.
-  uint4 ka[4], va[4], kb[4], vb[4];
-  issue(ka, va, entry(0), mine > 0);
-  int ph_next = entry(1);
-  // Scalar loads may return out of order, so waiting for one waits for all: each entry is
-  // requested only after the previous one has been consumed by issue().
-  for (int i = 0; i < mine; i += 2) {
-    issue(kb, vb, ph_next, i + 1 < mine);
-    const int ph2 = entry(i + 2);
-    process(ka, va, page_of(i));
-    if (i + 1 >= mine) break;
-    issue(ka, va, ph2, i + 2 < mine);
-    ph_next = entry(i + 3);
-    process(kb, vb, page_of(i + 1));
+  // Rotation over NBUF register buffers: pages i+1 .. i+NBUF-1 stream in while page i is
+  // computed.  Scalar loads may return out of order, so waiting for one waits for all: each
+  // block-table entry is requested only after the previous one has been consumed by issue().
+  uint4 kbuf[NBUF][4], vbuf[NBUF][4];
+#pragma unroll
+  for (int t = 0; t < NBUF - 1; ++t) issue(kbuf[t], vbuf[t], entry(t), t < mine);
+  int ph_next = entry(NBUF - 1);
+  for (int i = 0; i < mine; i += NBUF) {
+#pragma unroll
+    for (int t = 0; t < NBUF; ++t) {
+      const int ahead = i + t + NBUF - 1;
+      issue(kbuf[(t + NBUF - 1) % NBUF], vbuf[(t + NBUF - 1) % NBUF], ph_next, ahead < mine);
+      ph_next = entry(ahead + 1);
+      if (i + t >= mine) goto swept;
+      process(kbuf[t], vbuf[t], page_of(i + t));
+    }
   }
+swept:
 
   // Merge the 4 rows of the wavefront (lanes col, col+16, col+32, col+48 hold the same dims).
 #pragma unroll
@@ -282,12 +288,14 @@ decode_split_kernel(const uint16_t* __restrict__ qp, const uint16_t* __restrict_
         L = fmaf(f, s_l[w][h], L);
         A = fmaf(f, s_acc[w][h][d], A);
       }
-      out_o[(slot + h) * D + d] = A / L;
+      // Non-temporal: a thin stream of default-policy writes interleaved with the sweep's
+      // reads costs far more HBM time than its bytes (measured ~4% of the sweep).
+      __builtin_nontemporal_store(A / L, &out_o[(slot + h) * D + d]);
     }
     if (d == 0) {
       float lse = (M == -INFINITY) ? -INFINITY : (M + log2f(L)) * kLn2;
       if (bad) lse = NAN;
-      out_lse[slot + h] = lse;
+      __builtin_nontemporal_store(lse, &out_lse[slot + h]);
     }
   }
 }
@@ -295,7 +303,7 @@ decode_split_kernel(const uint16_t* __restrict__ qp, const uint16_t* __restrict_
 template <int G>
 hipError_t launch_g(const SplitParams& p, hipStream_t stream) {
   const unsigned grid = 8u * (unsigned)p.units_per_xcd;
-  hipLaunchKernelGGL((decode_split_kernel<G, kSplitWaves>), dim3(grid), dim3(64 * kSplitWaves),
+  hipLaunchKernelGGL((decode_split_kernel<G, kSplitWaves, kSplitBuffers>), dim3(grid), dim3(64 * kSplitWaves),
                      0, stream, p.q, p.k, p.v, p.block_table, p.ctx_lens, p.n_shards, p.out_o,
                      p.out_lse, p.hq, p.hkv, p.max_pages, p.num_pages, p.max_shards, p.chunks,
                      p.n_units, p.units_per_xcd, p.scale_log2);

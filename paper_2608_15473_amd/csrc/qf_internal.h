@@ -9,6 +9,7 @@ namespace qf {
 constexpr int kHeadDim = 128;     // D
 constexpr int kPage = 16;         // P
 constexpr int kSplitWaves = 4;    // waves per workgroup of the sweep kernel
+constexpr int kSplitBuffers = 2;  // pages in registers per wave (1 computed, the rest in flight)
 constexpr int kMergeWaves = 4;    // waves per workgroup of the merge kernel
 
 // One launch of the sweep kernel.  A workgroup handles one unit (request b, shard s, chunk c,

@@ -2,9 +2,11 @@
 on the same bytes, and apply the gates.
 
 Gates (floating point; derivation in the design doc):
-  * combined output (bf16): must be one of the two bf16 neighbours of the exact value (round to
-    nearest from an fp32 value within a few ulp of exact), which implies the contract bound
-    max|out - O| <= 2e-2; the contract bound is checked as well.
+  * combined output (bf16): the kernel rounds an fp32 value to nearest bf16; that fp32 value
+    may differ from the exact O by the fp32 accumulation error, allowed up to
+    delta = 1e-4 * max|O| per (request, head).  So out must lie between the bf16 value just below
+    O - delta and the bf16 value just above O + delta.  The contract bound max|out - O| <= 2e-2
+    is checked as well.
   * log-sum-exp (fp32), combined and per shard: |lse - LSE| <= 1e-5 * max(1, |LSE|).
   * per-shard O (fp32): max|O_s - O_s*| <= 1e-4 * max|O_s*| per (request, head).
   * empty shards: lse exactly -inf; all-empty requests: out exactly +0 and lse -inf.
@@ -108,7 +110,7 @@ def check(case, got, ref, pairs=None, label=""):
     """Apply every gate; returns a dict of the worst errors."""
     B, Hq, Hkv, D = case.shape
     todo = pairs if pairs is not None else [(b, h) for b in range(B) for h in range(Hq)]
-    worst = dict(out_abs=0.0, lse_rel=0.0, part_rel=0.0, part_lse_rel=0.0)
+    worst = dict(out_abs=0.0, out_rel=0.0, lse_rel=0.0, part_rel=0.0, part_lse_rel=0.0)
     for b, h in todo:
         O, L = ref["out"][b, h], ref["lse"][b, h]
         o, l = got["out"][b, h], got["lse"][b, h]
@@ -120,9 +122,13 @@ def check(case, got, ref, pairs=None, label=""):
             rel = abs(l - L) / max(1.0, abs(L))
             assert rel <= LSE_REL, (label, b, h, l, L)
             worst["lse_rel"] = max(worst["lse_rel"], rel)
-            lo, hi = bf16_neighbours(O)
-            ok = (o == lo) | (o == hi)
+            delta = PART_REL * float(np.max(np.abs(O)))
+            lo, _ = bf16_neighbours(O - delta)
+            _, hi = bf16_neighbours(O + delta)
+            ok = (o >= lo) & (o <= hi)
             assert ok.all(), (label, b, h, np.flatnonzero(~ok)[:5], o[~ok][:5], O[~ok][:5])
+            worst["out_rel"] = max(worst["out_rel"],
+                                   float(np.max(np.abs(o - O))) / float(np.max(np.abs(O))))
             err = float(np.max(np.abs(o - O)))
             assert err <= OUT_ABS
             worst["out_abs"] = max(worst["out_abs"], err)
