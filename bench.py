@@ -50,6 +50,25 @@ def algorithmic_bytes(case):
     return dict(kv=kv, sweep=sweep, combine=combine, attended=int(n.sum()))
 
 
+def committed_traffic(workload):
+    """HBM bytes per sweep launch from the committed rocprofv3 counter summary of this workload,
+    or None when there is none or the sweep kernel's sources changed since it was taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", f"decode_split_{workload}_hbm_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    h = hashlib.sha256()
+    for name in ("decode_split.hip", "qf_internal.h"):
+        with open(os.path.join(ROOT, "paper_2608_15473_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest() != rec.get("kernel_source_sha256"):
+        return None
+    return rec["traffic_bytes_per_launch"]
+
+
 def cpu_baseline(cases, budget_s=15.0):
     """The fp64 oracle (sweep per shard + pairwise merge) timed on the host over a bounded sample:
     whole requests, layer after layer, added until about ``budget_s`` of CPU work.  Device-to-host
@@ -204,7 +223,8 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "kernel": "decode_split_kernel", "launch_avg_us": round(sweep_avg_s * 1e6, 2),
-                     "traffic": None},
+                     "algorithmic_bytes": int(sweep_bytes),
+                     "traffic": committed_traffic(w.name) if L == w.layers else None},
     }
     if not args.no_cpu_baseline:
         log("[bench] cpu_baseline: timing the fp64 oracle on a bounded sample")
