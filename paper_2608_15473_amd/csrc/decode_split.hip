@@ -68,17 +68,36 @@ decode_split_kernel(const uint16_t* __restrict__ qp, const uint16_t* __restrict_
                     const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ n_shards,
                     float* __restrict__ out_o, float* __restrict__ out_lse, int32_t hq,
                     int32_t hkv, int32_t max_pages, int32_t num_pages, int32_t max_shards,
-                    int32_t chunks, int32_t n_units, int32_t units_per_xcd, float scale_log2) {
-  // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a contiguous range of
-  // units so the KV heads of one (request, shard) share that XCD's L2 for the block table.
-  const int unit = (int)(blockIdx.x % 8u) * units_per_xcd + (int)(blockIdx.x / 8u);
-  if (unit >= n_units) return;
-  const int g = unit % hkv;
-  int rest = unit / hkv;
-  const int c = rest % chunks;
-  rest /= chunks;
-  const int s = rest % max_shards;
-  const int b = rest / max_shards;
+                    int32_t chunks, int32_t n_units, int32_t units_per_xcd, int32_t batch,
+                    int32_t order, float scale_log2) {
+  // Which unit this workgroup sweeps.  Workgroups are dispatched in index order, round-robin over
+  // the 8 XCDs.
+  //  * Short shards (kOrderByRequest): each XCD takes a contiguous range of units in (request,
+  //    shard, chunk, KV head) order, so a request's query, context length and block-table lines
+  //    stay in one XCD's L2 and the short workgroups' prologues hit there.
+  //  * Long shards (kOrderByShardDesc): units in (shard descending, request, chunk, KV head) order,
+  //    round-robin over the XCDs, so the largest shards (high indices exist only in long requests)
+  //    start first and every XCD gets an even share; the small shards fill the tail.
+  int g, c, s, b;
+  if (order == kOrderByRequest) {
+    const int unit = (int)(blockIdx.x % 8u) * units_per_xcd + (int)(blockIdx.x / 8u);
+    if (unit >= n_units) return;
+    g = unit % hkv;
+    int rest = unit / hkv;
+    c = rest % chunks;
+    rest /= chunks;
+    s = rest % max_shards;
+    b = rest / max_shards;
+  } else {
+    const int unit = (int)blockIdx.x;
+    if (unit >= n_units) return;
+    g = unit % hkv;
+    int rest = unit / hkv;
+    c = rest % chunks;
+    rest /= chunks;
+    b = rest % batch;
+    s = max_shards - 1 - rest / batch;
+  }
 
   // The request's shape, checked: an out-of-range value is clamped (so nothing is read out of
   // bounds) and poisons this unit's log-sum-exp with NaN.
@@ -214,16 +233,17 @@ decode_split_kernel(const uint16_t* __restrict__ qp, const uint16_t* __restrict_
     }
   };
 
-  // The query loads must have landed before the loop, so that the only loads in flight inside it
-  // are the two page buffers (vmcnt 0, expcnt 7, lgkmcnt 15).
-  __builtin_amdgcn_s_waitcnt(0x0F70);
-
   // Rotation over NBUF register buffers: pages i+1 .. i+NBUF-1 stream in while page i is
   // computed.  Scalar loads may return out of order, so waiting for one waits for all: each
   // block-table entry is requested only after the previous one has been consumed by issue().
   uint4 kbuf[NBUF][4], vbuf[NBUF][4];
 #pragma unroll
   for (int t = 0; t < NBUF - 1; ++t) issue(kbuf[t], vbuf[t], entry(t), t < mine);
+  // The query loads (issued first) must have landed before the loop, so that the only loads in
+  // flight inside it are the page buffers; the first pages stay in flight meanwhile
+  // (s_waitcnt vmcnt(8 * (NBUF - 1)), expcnt 7, lgkmcnt 15).
+  constexpr int kAhead = 8 * (NBUF - 1);
+  __builtin_amdgcn_s_waitcnt((kAhead & 0xF) | ((kAhead >> 4) << 14) | 0x0F70);
   int ph_next = entry(NBUF - 1);
   for (int i = 0; i < mine; i += NBUF) {
 #pragma unroll
@@ -306,7 +326,7 @@ hipError_t launch_g(const SplitParams& p, hipStream_t stream) {
   hipLaunchKernelGGL((decode_split_kernel<G, kSplitWaves, kSplitBuffers>), dim3(grid), dim3(64 * kSplitWaves),
                      0, stream, p.q, p.k, p.v, p.block_table, p.ctx_lens, p.n_shards, p.out_o,
                      p.out_lse, p.hq, p.hkv, p.max_pages, p.num_pages, p.max_shards, p.chunks,
-                     p.n_units, p.units_per_xcd, p.scale_log2);
+                     p.n_units, p.units_per_xcd, p.batch, p.order, p.scale_log2);
   return hipGetLastError();
 }
 

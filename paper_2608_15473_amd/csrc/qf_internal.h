@@ -12,6 +12,12 @@ constexpr int kSplitWaves = 4;    // waves per workgroup of the sweep kernel
 constexpr int kSplitBuffers = 2;  // pages in registers per wave (1 computed, the rest in flight)
 constexpr int kMergeWaves = 4;    // waves per workgroup of the merge kernel
 
+// Dispatch orders of the sweep's units (see decode_split.hip).
+constexpr int kOrderByRequest = 0;
+constexpr int kOrderByShardDesc = 1;
+// Shards at least this long (pages, at full capacity) are swept in kOrderByShardDesc.
+constexpr int kLongShardPages = 128;
+
 // One launch of the sweep kernel.  A workgroup handles one unit (request b, shard s, chunk c,
 // KV head g); its output slot is [((b * max_shards + s) * chunks + c) * hq + g * G + h].
 struct SplitParams {
@@ -26,6 +32,7 @@ struct SplitParams {
   int32_t batch, hq, hkv, max_pages, num_pages, max_shards, chunks;
   int32_t n_units;              // B * max_shards * chunks * Hkv
   int32_t units_per_xcd;        // ceil(n_units / 8)
+  int32_t order;                // kOrderByRequest or kOrderByShardDesc (dispatch order of units)
   float scale_log2;             // softmax scale * log2(e)
 };
 

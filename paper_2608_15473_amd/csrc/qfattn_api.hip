@@ -140,6 +140,10 @@ int qf_attn_decode_split(const qf_decode_desc* desc, const void* q, const void* 
   p.chunks = (int32_t)chunks;
   p.n_units = (int32_t)units;
   p.units_per_xcd = (int32_t)((units + 7) / 8);
+  // Long shards: long-lived workgroups, the dispatch order decides the tail (largest first).
+  // Short shards: short workgroups, prologue latency decides (keep a request on one XCD).
+  const int64_t shard_pages = (d.max_pages_per_seq + d.max_shards - 1) / d.max_shards / chunks;
+  p.order = shard_pages >= qf::kLongShardPages ? qf::kOrderByShardDesc : qf::kOrderByRequest;
   p.scale_log2 = (float)((double)d.softmax_scale * 1.4426950408889634);
 
   hipStream_t s = static_cast<hipStream_t>(stream);

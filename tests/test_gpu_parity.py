@@ -65,6 +65,20 @@ def test_chunked_path(gpu):
     _run(case, "chunked")
 
 
+def test_ragged_batch_long_shards(gpu):
+    """A ragged batch whose shards are long enough (>= 128 pages at capacity) for the sweep to
+    dispatch its units largest-shard-first; includes empty requests and partial last pages."""
+    rng = np.random.default_rng(180)
+    n = np.rint(np.exp(rng.uniform(np.log(16), np.log(8192), size=64))).astype(int)
+    n[[3, 17]] = 0
+    S = np.maximum(1, -(-n // 4096))
+    case = make_case(64, 16, 8, n, S, seed=180, max_shards=4, max_pages=512, device=gpu)
+    order = np.argsort(n)
+    pairs = [(int(order[i]), h) for i, h in [(0, 0), (10, 5), (40, 9), (62, 14), (63, 15)]]
+    got, ref = _run(case, "ragged long shards", pairs)
+    assert np.all(got["part_lse"][[3, 17]] == -np.inf)
+
+
 def test_physical_page_placement_is_bitwise_irrelevant(gpu):
     """The same logical cache stored contiguously or scattered over a permuted pool gives
     bitwise identical results."""
