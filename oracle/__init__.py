@@ -28,4 +28,6 @@ from .attention import (  # noqa: F401
     merge_pair,
     fold_combine,
     combine_max_shifted,
+    fold_current,
+    append_kv,
 )

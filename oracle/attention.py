@@ -271,3 +271,60 @@ def combine_max_shifted(part_out, part_lse):
             out[b, h] = (w @ part_out[b, live, h, :]) / np.sum(w)
             lse[b, h] = m + np.log(np.sum(w))
     return out, lse
+
+
+# --------------------------------------------------------------------------------------------
+# the current token (§2 protocol table and combine, Appendix A fold) and the cache append
+# --------------------------------------------------------------------------------------------
+def fold_current(O_prev, lse_prev, q, k_cur, v_cur, scale: float):
+    """Fold the current token into the cache's (o_<j, lse_<j) for every request and query head.
+
+    §2 and Appendix A: s_jj = scale * q_j . k_j, out = lerp(v_j, o_<j, sigma(lse_<j - s_jj)),
+    lse = logaddexp(lse_<j, s_jj).  The cached history acts as one pseudo-token of score lse_<j
+    and value o_<j, so this is a two-way softmax.  An empty cache (lse_<j = -inf) gives
+    (v_j, s_jj) and its o_<j is not read.
+
+    O_prev [B, Hq, D], lse_prev [B, Hq], q [B, Hq, D], k_cur / v_cur [B, Hkv, D] (query head h
+    uses KV head h // (Hq / Hkv)).  Returns float64 (out [B, Hq, D], lse [B, Hq]).
+    """
+    O_prev = np.asarray(O_prev, dtype=np.float64)
+    lse_prev = np.asarray(lse_prev, dtype=np.float64)
+    q = np.asarray(q, dtype=np.float64)
+    k_cur = np.asarray(k_cur, dtype=np.float64)
+    v_cur = np.asarray(v_cur, dtype=np.float64)
+    B, Hq, D = q.shape
+    G = Hq // k_cur.shape[1]
+    out = np.zeros((B, Hq, D))
+    lse = np.zeros((B, Hq))
+    for b in range(B):
+        for h in range(Hq):
+            g = h // G
+            s_jj = float(scale) * float(q[b, h] @ k_cur[b, g])
+            if lse_prev[b, h] == NEG_INF:
+                out[b, h], lse[b, h] = v_cur[b, g], s_jj
+                continue
+            t = _sigmoid(lse_prev[b, h] - s_jj)
+            out[b, h] = (1.0 - t) * v_cur[b, g] + t * O_prev[b, h]
+            lse[b, h] = float(np.logaddexp(lse_prev[b, h], s_jj))
+    return out, lse
+
+
+def append_kv(k_cache, v_cache, block_table, ctx_lens, k_new, v_new, page_size: int = 16,
+              max_pages: int | None = None):
+    """The cache write of §2 (k_j and v_j appended, a write nothing waits on): returns copies of
+    the caches with request b's new key/value stored at its position n_b = ctx_lens[b], i.e.
+    physical page block_table[b, n_b // P], slot n_b % P, for every KV head."""
+    k = np.array(k_cache, copy=True)
+    v = np.array(v_cache, copy=True)
+    B = len(ctx_lens)
+    if max_pages is None:
+        max_pages = (np.asarray(block_table).shape[1] if block_table is not None
+                     else k.shape[0] // B)
+    for b in range(B):
+        n = int(ctx_lens[b])
+        page = int(_table_row(block_table, b, max_pages)[n // page_size])
+        if not 0 <= page < k.shape[0]:
+            raise ValueError(f"request {b}: no page allocated for position {n}")
+        k[page, :, n % page_size, :] = k_new[b]
+        v[page, :, n % page_size, :] = v_new[b]
+    return k, v

@@ -400,3 +400,76 @@ def test_planted_logits_overflow_naive_float32_and_oracle_stays_finite():
     fo, fl = oracle.fold_combine(po, pl, rng=np.random.default_rng(3))
     np.testing.assert_allclose(fo, out, rtol=1e-11, atol=1e-14)
     np.testing.assert_allclose(fl, lse, rtol=1e-14)
+
+
+# ------------------------------------------------------------------------------------------------
+# the current token: fold and append (§2, Appendix A)
+# ------------------------------------------------------------------------------------------------
+def _with_current(case_np, k_new, v_new):
+    """Attention over the cache plus the current token, by appending it and sweeping n + 1
+    positions with the plain definition (an independent path to the fold)."""
+    kc, vc = oracle.append_kv(case_np["k_cache"], case_np["v_cache"], case_np["block_table"],
+                              case_np["ctx_lens"], k_new, v_new)
+    return oracle.decode_unsplit(case_np["q"], kc, vc, case_np["block_table"],
+                                 case_np["ctx_lens"] + 1, SCALE)
+
+
+def test_fold_equals_attention_over_cache_plus_current():
+    # pages are allocated for n + 1 positions; the cache then holds n of them
+    case = make_case(3, 8, 2, [101, 2, 1], [3, 1, 1], seed=20, max_pages=8, head_dim=32)
+    case.ctx_lens -= 1
+    a = _as_np(case)
+    rng = np.random.default_rng(21)
+    k_new, v_new = _bf16(rng, 3, 2, 32), _bf16(rng, 3, 2, 32)
+    O, lse = oracle.decode_unsplit(a["q"], a["k_cache"], a["v_cache"], a["block_table"],
+                                   a["ctx_lens"], SCALE)
+    fo, fl = oracle.fold_current(O, lse, a["q"], k_new, v_new, SCALE)
+    ro, rl = _with_current(a, k_new, v_new)
+    np.testing.assert_allclose(fo, ro, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(fl, rl, rtol=1e-13)
+    # empty cache (request 2): the result is the current token alone
+    for h in range(8):
+        np.testing.assert_array_equal(fo[2, h], v_new[2, h // 4])
+        assert fl[2, h] == pytest.approx(SCALE * math.fsum(a["q"][2, h] * k_new[2, h // 4]))
+
+
+@pytest.mark.parametrize("gap", [-120.0, -30.0, -9.7, 0.0, 9.7, 30.0, 120.0])
+def test_fold_handles_either_sign_of_the_gap(gap):
+    """Appendix E: s_jj may exceed lse_<j (short caches), so the fold must work for both signs.
+    Expected weights from scipy's expit; the lse from the exactly rounded two-term sum."""
+    rng = np.random.default_rng(22)
+    D = 16
+    O_prev = _bf16(rng, 1, 1, D)
+    q = np.zeros((1, 1, D)); q[0, 0, 0] = 1.0
+    lse_prev = np.array([[5.0]])
+    k = np.zeros((1, 1, D)); k[0, 0, 0] = (5.0 + gap) / 0.25
+    v = _bf16(rng, 1, 1, D)
+    fo, fl = oracle.fold_current(O_prev, lse_prev, q, k, v, 0.25)
+    w_cur = scipy.special.expit(gap)                       # weight of the current token
+    np.testing.assert_allclose(fo[0, 0], (1 - w_cur) * O_prev[0, 0] + w_cur * v[0, 0],
+                               rtol=1e-13, atol=1e-15)
+    m = max(5.0, 5.0 + gap)
+    assert fl[0, 0] == pytest.approx(m + math.log(math.fsum([math.exp(5.0 - m),
+                                                             math.exp(5.0 + gap - m)])), rel=1e-14)
+
+
+def test_append_writes_only_the_new_slot():
+    case = make_case(2, 4, 2, [18, 32], [1, 1], seed=23, max_pages=4, head_dim=8)
+    case.ctx_lens -= 1
+    a = _as_np(case)
+    rng = np.random.default_rng(24)
+    k_new, v_new = _bf16(rng, 2, 2, 8), _bf16(rng, 2, 2, 8)
+    kc, vc = oracle.append_kv(a["k_cache"], a["v_cache"], a["block_table"], a["ctx_lens"],
+                              k_new, v_new)
+    changed = np.argwhere(np.any(kc != a["k_cache"], axis=-1))
+    want = {(int(a["block_table"][b, n // PAGE]), g, n % PAGE)
+            for b, n in enumerate(a["ctx_lens"]) for g in range(2)}
+    assert {tuple(map(int, x)) for x in changed} <= want
+    for b, n in enumerate(a["ctx_lens"]):
+        page = a["block_table"][b, n // PAGE]
+        np.testing.assert_array_equal(kc[page, :, n % PAGE], k_new[b])
+        np.testing.assert_array_equal(vc[page, :, n % PAGE], v_new[b])
+    bad = a["block_table"].copy()
+    bad[0, 1] = -1
+    with pytest.raises(ValueError):
+        oracle.append_kv(a["k_cache"], a["v_cache"], bad, a["ctx_lens"], k_new, v_new)
