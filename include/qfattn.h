@@ -116,6 +116,45 @@ int qf_attn_combine(int32_t batch, int32_t n_q_heads, int32_t head_dim, int32_t 
                     const float* part_out, const float* part_lse, void* out, float* lse,
                     void* stream);
 
+/*
+ * The merge above followed by the current token (§2 protocol table and combine; Appendix A fold):
+ * with (o_<j, lse_<j) the merge of the shard slots of request b and query head h,
+ *
+ *     s_jj = scale * q_j . k_j,   out = lerp(v_j, o_<j, sigma(lse_<j - s_jj)),
+ *     lse  = logaddexp(lse_<j, s_jj),   sigma(x) = 1 / (1 + exp(-x)),
+ *
+ * i.e. attention over the cached positions plus the current one.  Correct for either sign of
+ * s_jj - lse_<j (short caches, Appendix E) and for an empty cache (out = v_j, lse = s_jj).
+ *
+ *   q           bf16 [B, Hq, D] (the same query the sweep used), 4-byte aligned.
+ *   k_cur,v_cur bf16 [B, Hkv, D]: the current token's key and value; query head h uses KV head
+ *               h / G.  4-byte aligned.
+ *   part_out, part_lse, out, lse as for qf_attn_combine.  head_dim must be 128.
+ */
+int qf_attn_combine_current(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                            int32_t max_shards, const float* part_out, const float* part_lse,
+                            const void* q, const void* k_cur, const void* v_cur,
+                            float softmax_scale, void* out, float* lse, void* stream);
+
+/*
+ * The cache write of §2: k_j and v_j of every request are stored at its position n_b = ctx_lens[b],
+ * i.e. physical page block_table[b * max_pages_per_seq + n_b / P] (identity map when NULL), slot
+ * n_b % P, for every KV head.  The page must already belong to the request.
+ *
+ *   desc        as for qf_attn_decode_split (batch, n_kv_heads, head_dim, page_size,
+ *               max_pages_per_seq, num_pages are used).
+ *   k_cache,
+ *   v_cache     bf16 [num_pages, Hkv, P, D], written in place; 4-byte aligned.
+ *   ctx_lens    int32 [B]; when advance != 0, ctx_lens[b] becomes n_b + 1 after the write.
+ *   k_new,v_new bf16 [B, Hkv, D]; 4-byte aligned.
+ *   status      optional int32 device word: set to 1 (never cleared) when a request's append is
+ *               skipped because n_b is outside [0, max_pages_per_seq * P) or its page is outside
+ *               the pool; such a request's cache and ctx_lens are left unchanged.
+ */
+int qf_kv_append(const qf_decode_desc* desc, void* k_cache, void* v_cache,
+                 const int32_t* block_table, int32_t* ctx_lens, const void* k_new,
+                 const void* v_new, int32_t advance, int32_t* status, void* stream);
+
 /* Message for the last error on the calling thread; "" if none.  Valid until the thread's next
  * call into the library. */
 const char* qf_last_error(void);

@@ -16,8 +16,10 @@ from .binding import (  # noqa: F401
     DecodeDesc,
     QFError,
     attn_combine,
+    attn_combine_current,
     attn_decode,
     attn_decode_split,
+    kv_append,
     load_library,
     make_desc,
     workspace_size,

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(_HERE, "lib", "libqfattn.so")
 
 QF_OK, QF_EINVAL, QF_EUNSUPPORTED, QF_EALIGN, QF_EHIP = 0, -1, -2, -3, -4
 EXPORTED = ("qf_attn_decode_split_workspace_size", "qf_attn_decode_split", "qf_attn_combine",
-            "qf_last_error", "qf_version")
+            "qf_attn_combine_current", "qf_kv_append", "qf_last_error", "qf_version")
 
 
 class QFError(RuntimeError):
@@ -52,11 +52,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.qf_attn_decode_split.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp, vp, vp,
                                          vp, vp, sz, vp]
     lib.qf_attn_combine.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp]
+    lib.qf_attn_combine_current.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, vp,
+                                            ctypes.c_float, vp, vp, vp]
+    lib.qf_kv_append.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp, vp, i32, vp, vp]
     lib.qf_last_error.restype = ctypes.c_char_p
     lib.qf_last_error.argtypes = []
     lib.qf_version.argtypes = []
     for name in ("qf_attn_decode_split_workspace_size", "qf_attn_decode_split",
-                 "qf_attn_combine", "qf_version"):
+                 "qf_attn_combine", "qf_attn_combine_current", "qf_kv_append", "qf_version"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -162,6 +165,56 @@ def attn_combine(part_out, part_lse, out=None, lse=None, want_lse=True):
     _check(load_library().qf_attn_combine(B, Hq, D, S, _ptr(part_out), _ptr(part_lse), _ptr(out),
                                           _ptr(lse), ctypes.c_void_p(stream)))
     return out, lse
+
+
+def attn_combine_current(part_out, part_lse, q, k_cur, v_cur, scale=None, out=None, lse=None):
+    """Merge the shard slots, then fold in the current token (qf_attn_combine_current):
+    returns (out bf16 [B, Hq, D], lse fp32 [B, Hq]) = attention over cache + current token."""
+    _require(part_out, "part_out", torch.float32, 4)
+    _require(part_lse, "part_lse", torch.float32, 3)
+    _require(q, "q", torch.bfloat16, 3)
+    _require(k_cur, "k_cur", torch.bfloat16, 3)
+    _require(v_cur, "v_cur", torch.bfloat16, 3)
+    B, S, Hq, D = part_out.shape
+    Hkv = k_cur.shape[1]
+    if tuple(q.shape) != (B, Hq, D) or tuple(k_cur.shape) != (B, Hkv, D) or v_cur.shape != k_cur.shape:
+        raise QFError(QF_EINVAL, "q / k_cur / v_cur shapes do not match the partials")
+    if scale is None:
+        scale = D ** -0.5
+    if out is None:
+        out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=part_out.device)
+    if lse is None:
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=part_out.device)
+    stream = torch.cuda.current_stream(part_out.device).cuda_stream
+    _check(load_library().qf_attn_combine_current(
+        B, Hq, Hkv, D, S, _ptr(part_out), _ptr(part_lse), _ptr(q), _ptr(k_cur), _ptr(v_cur),
+        float(scale), _ptr(out), _ptr(lse), ctypes.c_void_p(stream)))
+    return out, lse
+
+
+def kv_append(k_cache, v_cache, block_table, ctx_lens, k_new, v_new, advance=True, status=None,
+              max_pages=None):
+    """Write each request's current key/value at position ctx_lens[b] (qf_kv_append); with
+    ``advance`` the context lengths are incremented on the device after the write."""
+    _require(k_cache, "k_cache", torch.bfloat16, 4)
+    _require(v_cache, "v_cache", torch.bfloat16, 4)
+    _require(ctx_lens, "ctx_lens", torch.int32, 1)
+    _require(k_new, "k_new", torch.bfloat16, 3)
+    _require(v_new, "v_new", torch.bfloat16, 3)
+    if block_table is not None:
+        _require(block_table, "block_table", torch.int32, 2)
+    if status is not None:
+        _require(status, "status", torch.int32)
+    B = ctx_lens.shape[0]
+    Hkv, P, D = k_cache.shape[1], k_cache.shape[2], k_cache.shape[3]
+    if max_pages is None:
+        max_pages = block_table.shape[1] if block_table is not None else k_cache.shape[0] // max(B, 1)
+    desc = DecodeDesc(B, Hkv, Hkv, D, P, int(max_pages), int(k_cache.shape[0]), 1, 1.0)
+    stream = torch.cuda.current_stream(k_cache.device).cuda_stream
+    _check(load_library().qf_kv_append(ctypes.byref(desc), _ptr(k_cache), _ptr(v_cache),
+                                       _ptr(block_table), _ptr(ctx_lens), _ptr(k_new),
+                                       _ptr(v_new), 1 if advance else 0, _ptr(status),
+                                       ctypes.c_void_p(stream)))
 
 
 def attn_decode(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards=None,

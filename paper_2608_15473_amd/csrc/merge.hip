@@ -10,6 +10,11 @@
 //
 // One workgroup per (row, head); its wavefronts take the entries round-robin, every lane owns 2
 // of the 128 dims, and the wavefronts' sums meet in LDS (they share the same m, so no rescale).
+//
+// With the current token (CUR): the merged pair is the cache's (o_<j, lse_<j), and the current
+// token is folded in as §2 and Appendix A state it: s_jj = scale * q_j . k_j,
+// out = lerp(v_j, o_<j, sigma(lse_<j - s_jj)) with sigma(x) = 1 / (1 + exp(-x)), and
+// lse = logaddexp(lse_<j, s_jj).  An empty cache gives sigma(-inf) = 0, i.e. out = v_j.
 #include <math.h>
 
 #include "qf_internal.h"
@@ -33,11 +38,15 @@ __device__ __forceinline__ uint32_t bf16_rne(float f) {
   return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
 }
 
-template <bool BF16>
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+template <bool BF16, bool CUR>
 __global__ void __launch_bounds__(64 * W)
 merge_kernel(const float* __restrict__ in_o, const float* __restrict__ in_lse,
              void* __restrict__ out_o, float* __restrict__ out_lse, int32_t entries,
-             int32_t hq) {
+             int32_t hq, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cur,
+             const uint16_t* __restrict__ v_cur, int32_t hkv, float scale) {
   const int pair = blockIdx.x;
   const int r = pair / hq;
   const int h = pair % hq;
@@ -116,6 +125,23 @@ merge_kernel(const float* __restrict__ in_o, const float* __restrict__ in_lse,
     a.y /= Lt;
     lse_out = M + logf(Lt);
   }
+  if (CUR) {
+    const int g = h / (hq / hkv);
+    const uint32_t qw = reinterpret_cast<const uint32_t*>(q + ((size_t)r * hq + h) * D)[lane];
+    const uint32_t kw = reinterpret_cast<const uint32_t*>(k_cur + ((size_t)r * hkv + g) * D)[lane];
+    const uint32_t vw = reinterpret_cast<const uint32_t*>(v_cur + ((size_t)r * hkv + g) * D)[lane];
+    float dot = fmaf(bf16_lo(qw), bf16_lo(kw), bf16_hi(qw) * bf16_hi(kw));
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) dot += __shfl_xor(dot, o);
+    const float s_jj = dot * scale;
+    const float t = 1.0f / (1.0f + expf(-(lse_out - s_jj)));   // weight of the cached history
+    a.x = (1.0f - t) * bf16_lo(vw) + t * a.x;
+    a.y = (1.0f - t) * bf16_hi(vw) + t * a.y;
+    const float mx = fmaxf(lse_out, s_jj);
+    float joined = mx + log1pf(expf(-fabsf(lse_out - s_jj)));  // stabilised logaddexp
+    if (mx == -INFINITY) joined = -INFINITY;
+    lse_out = (lse_out != lse_out || s_jj != s_jj) ? NAN : joined;
+  }
   if (BF16) {
     reinterpret_cast<uint32_t*>(out_o)[out_idx] = bf16_rne(a.x) | (bf16_rne(a.y) << 16);
   } else if (M != -INFINITY || nan) {
@@ -129,12 +155,18 @@ merge_kernel(const float* __restrict__ in_o, const float* __restrict__ in_lse,
 hipError_t launch_merge(const MergeParams& p, bool to_bf16, hipStream_t stream) {
   const unsigned grid = (unsigned)p.rows * (unsigned)p.hq;
   if (grid == 0) return hipSuccess;
-  if (to_bf16)
-    hipLaunchKernelGGL(merge_kernel<true>, dim3(grid), dim3(64 * W), 0, stream, p.in_o,
-                       p.in_lse, p.out_o, p.out_lse, p.entries, p.hq);
+  if (p.q)
+    hipLaunchKernelGGL((merge_kernel<true, true>), dim3(grid), dim3(64 * W), 0, stream, p.in_o,
+                       p.in_lse, p.out_o, p.out_lse, p.entries, p.hq, p.q, p.k_cur, p.v_cur,
+                       p.hkv, p.scale);
+  else if (to_bf16)
+    hipLaunchKernelGGL((merge_kernel<true, false>), dim3(grid), dim3(64 * W), 0, stream, p.in_o,
+                       p.in_lse, p.out_o, p.out_lse, p.entries, p.hq, nullptr, nullptr, nullptr,
+                       1, 0.0f);
   else
-    hipLaunchKernelGGL(merge_kernel<false>, dim3(grid), dim3(64 * W), 0, stream, p.in_o,
-                       p.in_lse, p.out_o, p.out_lse, p.entries, p.hq);
+    hipLaunchKernelGGL((merge_kernel<false, false>), dim3(grid), dim3(64 * W), 0, stream, p.in_o,
+                       p.in_lse, p.out_o, p.out_lse, p.entries, p.hq, nullptr, nullptr, nullptr,
+                       1, 0.0f);
   return hipGetLastError();
 }
 

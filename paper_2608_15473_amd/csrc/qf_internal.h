@@ -39,13 +39,34 @@ struct SplitParams {
 // Merge of `entries` partial states per (row, head):
 //   in  O [rows, entries, hq, D] fp32, lse [rows, entries, hq] fp32 (natural log)
 //   out O [rows, hq, D] (fp32 or bf16), lse [rows, hq] fp32 (may be null)
+// With q non-null (final output only) the current token is folded in after the merge:
+//   q bf16 [rows, hq, D], k_cur / v_cur bf16 [rows, hkv, D].
 struct MergeParams {
   const float* in_o;
   const float* in_lse;
   void* out_o;
   float* out_lse;
   int32_t rows, entries, hq;
+  const uint16_t* q = nullptr;
+  const uint16_t* k_cur = nullptr;
+  const uint16_t* v_cur = nullptr;
+  int32_t hkv = 1;
+  float scale = 0.0f;
 };
+
+// Cache append: write the current token's key and value at position ctx_lens[b] of request b.
+struct AppendParams {
+  uint16_t* k;                  // bf16 [num_pages, Hkv, P, D]
+  uint16_t* v;
+  const int32_t* block_table;   // [B, max_pages] or null (identity)
+  int32_t* ctx_lens;            // [B]; advanced by one after the write when advance != 0
+  const uint16_t* k_new;        // bf16 [B, Hkv, D]
+  const uint16_t* v_new;
+  int32_t* status;              // optional: set to 1 when an append is skipped
+  int32_t batch, hkv, max_pages, num_pages, advance;
+};
+
+hipError_t launch_kv_append(const AppendParams& p, hipStream_t stream);
 
 hipError_t launch_decode_split(const SplitParams& p, int group, hipStream_t stream);
 // to_bf16 = false: partial-state output (fp32 O not written for an empty row);

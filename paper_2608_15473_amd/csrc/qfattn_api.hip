@@ -191,4 +191,77 @@ int qf_attn_combine(int32_t batch, int32_t n_q_heads, int32_t head_dim, int32_t 
   return QF_OK;
 }
 
+int qf_attn_combine_current(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                            int32_t max_shards, const float* part_out, const float* part_lse,
+                            const void* q, const void* k_cur, const void* v_cur,
+                            float softmax_scale, void* out, float* lse, void* stream) {
+  g_error[0] = 0;
+  if (batch < 0) return fail(QF_EINVAL, "batch %d < 0", batch);
+  if (n_q_heads < 1 || n_kv_heads < 1)
+    return fail(QF_EINVAL, "n_q_heads %d / n_kv_heads %d must be >= 1", n_q_heads, n_kv_heads);
+  if (n_q_heads % n_kv_heads != 0)
+    return fail(QF_EINVAL, "n_q_heads %d is not a multiple of n_kv_heads %d", n_q_heads, n_kv_heads);
+  if (max_shards < 1) return fail(QF_EINVAL, "max_shards %d < 1", max_shards);
+  if (head_dim != qf::kHeadDim) return fail(QF_EUNSUPPORTED, "head_dim %d != %d", head_dim, qf::kHeadDim);
+  if (!isfinite(softmax_scale)) return fail(QF_EINVAL, "softmax_scale is not finite");
+  if (batch == 0) return QF_OK;
+  if (!part_out || !part_lse || !out || !q || !k_cur || !v_cur)
+    return fail(QF_EINVAL, "a required pointer is NULL");
+  if (!aligned(part_out, 16)) return fail(QF_EALIGN, "part_out must be 16-byte aligned");
+  if (!aligned(part_lse, 4) || !aligned(out, 4) || (lse && !aligned(lse, 4)) || !aligned(q, 4) ||
+      !aligned(k_cur, 4) || !aligned(v_cur, 4))
+    return fail(QF_EALIGN, "part_lse, out, lse, q, k_cur and v_cur must be 4-byte aligned");
+  if ((int64_t)batch * n_q_heads > INT32_MAX) return fail(QF_EINVAL, "batch * n_q_heads too large");
+  qf::MergeParams m{};
+  m.in_o = part_out;
+  m.in_lse = part_lse;
+  m.out_o = out;
+  m.out_lse = lse;
+  m.rows = batch;
+  m.entries = max_shards;
+  m.hq = n_q_heads;
+  m.q = static_cast<const uint16_t*>(q);
+  m.k_cur = static_cast<const uint16_t*>(k_cur);
+  m.v_cur = static_cast<const uint16_t*>(v_cur);
+  m.hkv = n_kv_heads;
+  m.scale = softmax_scale;
+  const hipError_t e = qf::launch_merge(m, true, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(QF_EHIP, "combine launch: %s", hipGetErrorString(e));
+  return QF_OK;
+}
+
+int qf_kv_append(const qf_decode_desc* desc, void* k_cache, void* v_cache,
+                 const int32_t* block_table, int32_t* ctx_lens, const void* k_new,
+                 const void* v_new, int32_t advance, int32_t* status, void* stream) {
+  g_error[0] = 0;
+  const int rc = check_desc(desc);
+  if (rc) return rc;
+  const qf_decode_desc& d = *desc;
+  if (d.batch == 0) return QF_OK;
+  if (!k_cache || !v_cache || !ctx_lens || !k_new || !v_new)
+    return fail(QF_EINVAL, "a required pointer is NULL");
+  if (!aligned(k_cache, 4) || !aligned(v_cache, 4) || !aligned(k_new, 4) || !aligned(v_new, 4) ||
+      !aligned(ctx_lens, 4) || (block_table && !aligned(block_table, 4)) ||
+      (status && !aligned(status, 4)))
+    return fail(QF_EALIGN, "cache, new-token, index and status pointers must be 4-byte aligned");
+  if (!block_table && (int64_t)d.batch * d.max_pages_per_seq > d.num_pages)
+    return fail(QF_EINVAL, "identity block table needs num_pages >= batch * max_pages_per_seq");
+  qf::AppendParams p{};
+  p.k = static_cast<uint16_t*>(k_cache);
+  p.v = static_cast<uint16_t*>(v_cache);
+  p.block_table = block_table;
+  p.ctx_lens = ctx_lens;
+  p.k_new = static_cast<const uint16_t*>(k_new);
+  p.v_new = static_cast<const uint16_t*>(v_new);
+  p.status = status;
+  p.batch = d.batch;
+  p.hkv = d.n_kv_heads;
+  p.max_pages = d.max_pages_per_seq;
+  p.num_pages = d.num_pages;
+  p.advance = advance ? 1 : 0;
+  const hipError_t e = qf::launch_kv_append(p, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(QF_EHIP, "kv_append launch: %s", hipGetErrorString(e));
+  return QF_OK;
+}
+
 }  // extern "C"

@@ -124,6 +124,26 @@ def test_combine_rejects_bad_arguments():
     assert lib.qf_attn_combine(0, 16, 128, 4, None, None, None, None, None) == qf.QF_OK
 
 
+def test_current_token_entry_points_reject_bad_arguments():
+    lib = load_library()
+    a = ctypes.c_void_p(4096)
+    f = lib.qf_attn_combine_current
+    assert f(-1, 16, 8, 128, 4, a, a, a, a, a, 0.1, a, a, None) == qf.QF_EINVAL
+    assert f(2, 16, 6, 128, 4, a, a, a, a, a, 0.1, a, a, None) == qf.QF_EINVAL
+    assert f(2, 16, 8, 64, 4, a, a, a, a, a, 0.1, a, a, None) == qf.QF_EUNSUPPORTED
+    assert f(2, 16, 8, 128, 4, a, a, None, a, a, 0.1, a, a, None) == qf.QF_EINVAL
+    assert f(2, 16, 8, 128, 4, a, a, a, a, a, float("inf"), a, a, None) == qf.QF_EINVAL
+    assert f(2, 16, 8, 128, 4, a, a, ctypes.c_void_p(4098), a, a, 0.1, a, a, None) == qf.QF_EALIGN
+    assert f(0, 16, 8, 128, 4, None, None, None, None, None, 0.1, None, None, None) == qf.QF_OK
+    g = lib.qf_kv_append
+    d = _desc()
+    assert g(ctypes.byref(_desc(head_dim=64)), a, a, a, a, a, a, 1, None, None) == qf.QF_EUNSUPPORTED
+    assert g(ctypes.byref(d), None, a, a, a, a, a, 1, None, None) == qf.QF_EINVAL
+    assert g(ctypes.byref(d), a, a, a, a, ctypes.c_void_p(4099), a, 1, None, None) == qf.QF_EALIGN
+    assert g(ctypes.byref(_desc(num_pages=100)), a, a, None, a, a, a, 1, None, None) == qf.QF_EINVAL
+    assert g(ctypes.byref(_desc(batch=0)), None, None, None, None, None, None, 1, None, None) == 0
+
+
 def test_empty_batch_is_a_no_op():
     lib = load_library()
     d = _desc(batch=0)
