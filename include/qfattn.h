@@ -155,6 +155,34 @@ int qf_kv_append(const qf_decode_desc* desc, void* k_cache, void* v_cache,
                  const int32_t* block_table, int32_t* ctx_lens, const void* k_new,
                  const void* v_new, int32_t advance, int32_t* status, void* stream);
 
+/*
+ * Host-side simulation of the layer-wise decode schedule (Appendix D, the wiring as a schedule).
+ * Not a GPU call: every pointer here is a HOST pointer, and the call is synchronous.
+ *
+ * Request r arrives at arrival[r] and sweeps its cache for attn_time[r] at every layer.  Each
+ * layer's feed-forward is a pool serving one departure at a time; a departure takes ffn_time,
+ * carries every request then waiting, and leaves only with at least min_batch waiting, or when
+ * the oldest has waited max_wait (INFINITY: never; the paper's rule, under which a request can be
+ * stranded).
+ *   QF_WIRING_QFIRST:   e_1 = arrival + a, e_l = max(e_{l-1} + a, ffn_{l-1}), finish = ffn_L: at
+ *                       e_l the request joins pool l and starts the sweep of layer l+1.
+ *   QF_WIRING_COMPOSED: the request joins pool l when sweep l ends and sweeps layer l+1 when that
+ *                       feed-forward returns.
+ * At each instant every completion is applied before any pool decides whether to depart.
+ *
+ *   finish       double [n_requests]: return time of the last feed-forward; NaN if stranded.
+ *   sweep_start, sweep_end, ffn_depart, ffn_return
+ *                double [n_requests, n_layers] or NULL; NaN for what never happened.
+ * Returns QF_OK or QF_EINVAL (n_layers < 1, min_batch < 1, ffn_time <= 0, max_wait < 0 or NaN,
+ * non-finite arrival / attention time, negative attention time, unknown wiring).
+ */
+#define QF_WIRING_QFIRST 0
+#define QF_WIRING_COMPOSED 1
+int qf_schedule_simulate(int32_t n_requests, const double* arrival, const double* attn_time,
+                         int32_t n_layers, int32_t wiring, double ffn_time, int32_t min_batch,
+                         double max_wait, double* finish, double* sweep_start, double* sweep_end,
+                         double* ffn_depart, double* ffn_return);
+
 /* Message for the last error on the calling thread; "" if none.  Valid until the thread's next
  * call into the library. */
 const char* qf_last_error(void);

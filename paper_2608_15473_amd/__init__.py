@@ -21,6 +21,7 @@ from .binding import (  # noqa: F401
     attn_decode_split,
     kv_append,
     load_library,
+    schedule_simulate,
     make_desc,
     workspace_size,
 )

@@ -17,7 +17,9 @@ LIB_PATH = os.path.join(_HERE, "lib", "libqfattn.so")
 
 QF_OK, QF_EINVAL, QF_EUNSUPPORTED, QF_EALIGN, QF_EHIP = 0, -1, -2, -3, -4
 EXPORTED = ("qf_attn_decode_split_workspace_size", "qf_attn_decode_split", "qf_attn_combine",
-            "qf_attn_combine_current", "qf_kv_append", "qf_last_error", "qf_version")
+            "qf_attn_combine_current", "qf_kv_append", "qf_schedule_simulate", "qf_last_error",
+            "qf_version")
+QF_WIRING_QFIRST, QF_WIRING_COMPOSED = 0, 1
 
 
 class QFError(RuntimeError):
@@ -55,11 +57,15 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.qf_attn_combine_current.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, vp,
                                             ctypes.c_float, vp, vp, vp]
     lib.qf_kv_append.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp, vp, i32, vp, vp]
+    dp = ctypes.POINTER(ctypes.c_double)
+    lib.qf_schedule_simulate.argtypes = [i32, dp, dp, i32, i32, ctypes.c_double, i32,
+                                         ctypes.c_double, dp, dp, dp, dp, dp]
     lib.qf_last_error.restype = ctypes.c_char_p
     lib.qf_last_error.argtypes = []
     lib.qf_version.argtypes = []
     for name in ("qf_attn_decode_split_workspace_size", "qf_attn_decode_split",
-                 "qf_attn_combine", "qf_attn_combine_current", "qf_kv_append", "qf_version"):
+                 "qf_attn_combine", "qf_attn_combine_current", "qf_kv_append",
+                 "qf_schedule_simulate", "qf_version"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -224,3 +230,27 @@ def attn_decode(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards
                                max_shards=max_shards, scale=scale)
     out, lse = attn_combine(po, pl)
     return out, lse, po, pl
+
+
+def schedule_simulate(arrival, attn_time, n_layers, wiring="qfirst", ffn_time=1.0, min_batch=2,
+                      max_wait=float("inf")):
+    """Host simulation of the layer-wise decode schedule (qf_schedule_simulate).
+
+    Returns a dict of numpy float64 arrays: finish [R] (NaN = stranded), sweep_start, sweep_end,
+    ffn_depart, ffn_return [R, n_layers] (NaN = never happened)."""
+    import numpy as np
+
+    arr = np.ascontiguousarray(arrival, dtype=np.float64)
+    att = np.ascontiguousarray(attn_time, dtype=np.float64)
+    R = arr.shape[0]
+    if att.shape != (R,):
+        raise QFError(QF_EINVAL, "arrival and attn_time must have the same length")
+    w = {"qfirst": QF_WIRING_QFIRST, "composed": QF_WIRING_COMPOSED}[wiring]
+    out = {k: np.full((R, n_layers) if k != "finish" else (R,), np.nan)
+           for k in ("finish", "sweep_start", "sweep_end", "ffn_depart", "ffn_return")}
+    dptr = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+    _check(load_library().qf_schedule_simulate(
+        R, dptr(arr), dptr(att), int(n_layers), w, float(ffn_time), int(min_batch),
+        float(max_wait), dptr(out["finish"]), dptr(out["sweep_start"]), dptr(out["sweep_end"]),
+        dptr(out["ffn_depart"]), dptr(out["ffn_return"])))
+    return out

@@ -68,6 +68,12 @@ struct AppendParams {
 
 hipError_t launch_kv_append(const AppendParams& p, hipStream_t stream);
 
+// Host simulation of the layer-wise decode schedule (schedule.cpp).
+int simulate_schedule(int R, const double* arrival, const double* attn_time, int L, int wiring,
+                      double ffn_time, int min_batch, double max_wait, double* finish,
+                      double* sweep_start, double* sweep_end, double* ffn_depart,
+                      double* ffn_return);
+
 hipError_t launch_decode_split(const SplitParams& p, int group, hipStream_t stream);
 // to_bf16 = false: partial-state output (fp32 O not written for an empty row);
 // to_bf16 = true:  final output (bf16, +0 for an empty row).

@@ -264,4 +264,31 @@ int qf_kv_append(const qf_decode_desc* desc, void* k_cache, void* v_cache,
   return QF_OK;
 }
 
+int qf_schedule_simulate(int32_t n_requests, const double* arrival, const double* attn_time,
+                         int32_t n_layers, int32_t wiring, double ffn_time, int32_t min_batch,
+                         double max_wait, double* finish, double* sweep_start, double* sweep_end,
+                         double* ffn_depart, double* ffn_return) {
+  g_error[0] = 0;
+  if (n_requests < 0) return fail(QF_EINVAL, "n_requests %d < 0", n_requests);
+  if (n_layers < 1) return fail(QF_EINVAL, "n_layers %d < 1", n_layers);
+  if (min_batch < 1) return fail(QF_EINVAL, "min_batch %d < 1", min_batch);
+  if (wiring != QF_WIRING_QFIRST && wiring != QF_WIRING_COMPOSED)
+    return fail(QF_EINVAL, "wiring %d is neither QF_WIRING_QFIRST nor QF_WIRING_COMPOSED", wiring);
+  if (!(ffn_time > 0.0) || !isfinite(ffn_time))
+    return fail(QF_EINVAL, "ffn_time must be finite and > 0");
+  if (!(max_wait >= 0.0)) return fail(QF_EINVAL, "max_wait must be >= 0 (INFINITY: no time-out)");
+  if (n_requests == 0) return QF_OK;
+  if (!arrival || !attn_time || !finish) return fail(QF_EINVAL, "a required pointer is NULL");
+  for (int r = 0; r < n_requests; ++r)
+    if (!isfinite(arrival[r]) || !isfinite(attn_time[r]) || attn_time[r] < 0.0)
+      return fail(QF_EINVAL, "request %d: arrival and attention time must be finite, time >= 0", r);
+  if ((int64_t)n_requests * n_layers > (int64_t)INT32_MAX)
+    return fail(QF_EINVAL, "n_requests * n_layers too large");
+  const int rc = qf::simulate_schedule(n_requests, arrival, attn_time, n_layers, wiring, ffn_time,
+                                       min_batch, max_wait, finish, sweep_start, sweep_end,
+                                       ffn_depart, ffn_return);
+  if (rc) return fail(rc, "simulation failed (out of host memory?)");
+  return QF_OK;
+}
+
 }  // extern "C"
