@@ -8,8 +8,8 @@
 // ln Z = -inf is empty: its weight is selected to 0 and its O (possibly garbage, §5) is never
 // multiplied.  A NaN among the ln Z makes the row's output NaN.
 //
-// One workgroup per (row, head); its wavefronts take the entries round-robin, every lane owns 2
-// of the 128 dims, and the wavefronts' sums meet in LDS (they share the same m, so no rescale).
+// One workgroup per (row, head); its wavefronts take the entries in groups of 16, every lane owns
+// 2 of the 128 dims, and the wavefronts' sums meet in LDS.
 //
 // With the current token (CUR): the merged pair is the cache's (o_<j, lse_<j), and the current
 // token is folded in as §2 and Appendix A state it: s_jj = scale * q_j . k_j,
@@ -24,12 +24,6 @@ namespace {
 
 constexpr int D = kHeadDim;
 constexpr int W = kMergeWaves;
-
-__device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
-  return x;
-}
 
 // fp32 -> bf16, round to nearest even; NaN stays a (quiet) NaN.
 __device__ __forceinline__ uint32_t bf16_rne(float f) {
@@ -56,65 +50,77 @@ merge_kernel(const float* __restrict__ in_o, const float* __restrict__ in_lse,
   const float2* o = reinterpret_cast<const float2*>(in_o + ((size_t)r * entries * hq + h) * D) + lane;
   const size_t o_step = (size_t)hq * D / 2;  // float2 between entries
 
-  // m and the NaN flag over all entries, 64 entries per pass.
-  float M = -INFINITY;
-  int nan = 0;
-  for (int i0 = 0; i0 < entries; i0 += 64) {
-    const int i = i0 + lane;
-    const float x = (i < entries) ? lse[(size_t)i * hq] : -INFINITY;
-    nan |= (x != x);
-    M = fmaxf(M, x);
-  }
-  M = wave_max(M);
-  nan = __any(nan);
-
-  float2 acc = make_float2(0.0f, 0.0f);
+  // Wavefront w takes entries [K w, K w + K) of every K W.  Its K log-partitions and O rows are
+  // all loaded before any is used, so a row costs one memory round trip; each wavefront keeps its
+  // own running maximum m_w (rescaling its sums when a later group raises it), and the wavefronts
+  // meet in LDS, where every sum is rescaled by exp(m_w - m).  Empty entries are selected out.
+  constexpr int K = 16;
+  float m_w = -INFINITY;
   float L = 0.0f;
-  if (!nan && M != -INFINITY) {
-    // Groups of 4 entries per wavefront: the loads of a group are issued together; a group whose
-    // entries are all empty is skipped (unused shard slots sit at the end of a row).
-    for (int i0 = 4 * wave; i0 < entries; i0 += 4 * W) {
-      float x[4];
-      bool live = false;
+  float2 acc = make_float2(0.0f, 0.0f);
+  bool nan = false;
+  for (int i0 = K * wave; i0 < entries; i0 += K * W) {
+    float x[K];
+    float2 v[K];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        x[k] = (i0 + k < entries) ? lse[(size_t)(i0 + k) * hq] : -INFINITY;
-        live |= (x[k] != -INFINITY);
-      }
-      if (!live) continue;
-      float2 v[4];
+    for (int k = 0; k < K; ++k) {
+      const bool in = i0 + k < entries;
+      x[k] = in ? lse[(size_t)(i0 + k) * hq] : -INFINITY;
+      v[k] = in ? o[(size_t)(i0 + k) * o_step] : make_float2(0.0f, 0.0f);
+    }
+    float mc = m_w;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) v[k] = (i0 + k < entries) ? o[(size_t)(i0 + k) * o_step] : make_float2(0.0f, 0.0f);
+    for (int k = 0; k < K; ++k) {
+      nan |= (x[k] != x[k]);
+      mc = fmaxf(mc, x[k]);
+    }
+    if (mc == -INFINITY) continue;  // nothing live so far
+    const float f = (m_w == -INFINITY) ? 0.0f : expf(m_w - mc);
+    L *= f;
+    acc.x *= f;
+    acc.y *= f;
+    m_w = mc;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        if (x[k] != -INFINITY) {
-          const float w = expf(x[k] - M);
-          L += w;
-          acc.x = fmaf(w, v[k].x, acc.x);
-          acc.y = fmaf(w, v[k].y, acc.y);
-        }
-      }
+    for (int k = 0; k < K; ++k) {
+      const float w = (x[k] == -INFINITY) ? 0.0f : expf(x[k] - m_w);
+      L += w;
+      acc.x = (w == 0.0f) ? acc.x : fmaf(w, v[k].x, acc.x);
+      acc.y = (w == 0.0f) ? acc.y : fmaf(w, v[k].y, acc.y);
     }
   }
 
   __shared__ float2 s_acc[W][64];
   __shared__ float s_L[W];
+  __shared__ float s_m[W];
+  __shared__ int s_nan[W];
   s_acc[wave][lane] = acc;
-  if (lane == 0) s_L[wave] = L;
+  if (lane == 0) {
+    s_L[wave] = L;
+    s_m[wave] = m_w;
+    s_nan[wave] = nan;
+  }
   __syncthreads();
   if (wave != 0) return;
 
-  float2 a = s_acc[0][lane];
-  float Lt = s_L[0];
+  float M = s_m[0];
+  bool any_nan = s_nan[0];
 #pragma unroll
   for (int w = 1; w < W; ++w) {
-    a.x += s_acc[w][lane].x;
-    a.y += s_acc[w][lane].y;
-    Lt += s_L[w];
+    M = fmaxf(M, s_m[w]);
+    any_nan |= s_nan[w];
+  }
+  float2 a = make_float2(0.0f, 0.0f);
+  float Lt = 0.0f;
+#pragma unroll
+  for (int w = 0; w < W; ++w) {
+    const float f = (s_m[w] == -INFINITY) ? 0.0f : expf(s_m[w] - M);
+    a.x = fmaf(f, s_acc[w][lane].x, a.x);
+    a.y = fmaf(f, s_acc[w][lane].y, a.y);
+    Lt = fmaf(f, s_L[w], Lt);
   }
   float lse_out;
   const size_t out_idx = ((size_t)r * hq + h) * D / 2 + lane;  // float2 / bf16-pair index
-  if (nan) {
+  if (any_nan) {
     a = make_float2(NAN, NAN);
     lse_out = NAN;
   } else if (M == -INFINITY) {
@@ -144,7 +150,7 @@ merge_kernel(const float* __restrict__ in_o, const float* __restrict__ in_lse,
   }
   if (BF16) {
     reinterpret_cast<uint32_t*>(out_o)[out_idx] = bf16_rne(a.x) | (bf16_rne(a.y) << 16);
-  } else if (M != -INFINITY || nan) {
+  } else if (M != -INFINITY || any_nan) {
     reinterpret_cast<float2*>(out_o)[out_idx] = a;
   }
   if (out_lse && lane == 0) out_lse[(size_t)r * hq + h] = lse_out;
