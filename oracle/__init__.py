@@ -13,6 +13,8 @@ What it computes follows the paper (Q-First, arXiv:2608.15473):
   (O, log Z); two shards merge by lerp / sigmoid / logaddexp; an empty shard is log Z = -inf
   and its vector is never read.
 * §2 (score definition): s = q . k / sqrt(d); here the scale is passed in explicitly.
+* §2 and §8 (the rewired block): the query reads the block input u, the key and value the
+  post-feed-forward stream z = u + M(N2 u); the block's output is z + W_o attn (``block.py``).
 
 Every function works in float64 on exact copies of the bf16 inputs.  Parity status of each
 function is stated in its docstring; the pins live in ``tests/test_oracle_*.py``.
@@ -30,4 +32,12 @@ from .attention import (  # noqa: F401
     combine_max_shifted,
     fold_current,
     append_kv,
+)
+from .block import (  # noqa: F401
+    RMS_EPS,
+    rms_norm,
+    silu,
+    swiglu,
+    feed_forward,
+    qfirst_block,
 )

@@ -210,3 +210,80 @@ def workload_case(name: str, layer: int = 0, device="cpu", **override) -> Case:
         kw["planted"] = (400, 84.0, 86.0)
     kw.update(override)
     return make_case(w.batch, w.n_q_heads, w.n_kv_heads, lengths, w.shard_counts(lengths), **kw)
+
+
+# --------------------------------------------------------------------------------------------
+# Q-First decode blocks with synthetic weights (the [MLP || Attn] stage)
+# --------------------------------------------------------------------------------------------
+@dataclasses.dataclass(frozen=True)
+class BlockShape:
+    """Dense sizes of one decoder block (Qwen3 configurations; the byte table of the paper's §3 counts
+    19 MB of feed-forward weights per layer at Qwen3-0.6B and 149 MB at Qwen3-4B)."""
+    name: str
+    hidden: int
+    inter: int
+    n_q_heads: int
+    n_kv_heads: int
+    layers: int
+
+    def ffn_bytes(self) -> int:
+        return 3 * self.hidden * self.inter * 2
+
+
+BLOCKS = {
+    b.name: b
+    for b in [
+        BlockShape("qwen3-0.6b", hidden=1024, inter=3072, n_q_heads=16, n_kv_heads=8, layers=28),
+        BlockShape("qwen3-4b", hidden=2560, inter=9728, n_q_heads=32, n_kv_heads=8, layers=36),
+    ]
+}
+
+
+@dataclasses.dataclass(frozen=True)
+class StageWorkload:
+    """A decode step of a stack of blocks at the context where the feed-forward's weight bytes
+    equal the sweep's cache bytes (the crossover column of the byte table in the paper's §3)."""
+    name: str
+    index: int                 # seeds are 1000 * index + layer
+    block: str
+    batch: int
+    ctx: int
+    shards: int
+
+
+STAGE_WORKLOADS = {
+    w.name: w
+    for w in [
+        StageWorkload("qwen3-0.6b_stage_b1_n4608", 11, "qwen3-0.6b", batch=1, ctx=4608, shards=8),
+        StageWorkload("qwen3-4b_stage_b1_n36480", 12, "qwen3-4b", batch=1, ctx=36480, shards=32),
+    ]
+}
+
+
+def block_weights(shape: BlockShape, seed: int, head_dim: int = HEAD_DIM, device="cpu"):
+    """Seeded bf16 weights of one block, torch layout [out, in].
+
+    Draw order: W_q, W_k, W_v, W_o, W_gate, W_up, W_down (N(0, 1/fan_in), so activations stay
+    O(1)), then the two norm gains g1, g2 (U(0.5, 1.5))."""
+    H, I = shape.hidden, shape.inter
+    qd, kd = shape.n_q_heads * head_dim, shape.n_kv_heads * head_dim
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+
+    def mat(rows, cols):
+        w = torch.randn(rows, cols, generator=gen, device=device, dtype=torch.float32)
+        return (w * (1.0 / math.sqrt(cols))).to(torch.bfloat16)
+
+    w = {"w_q": mat(qd, H), "w_k": mat(kd, H), "w_v": mat(kd, H), "w_o": mat(H, qd),
+         "w_gate": mat(I, H), "w_up": mat(I, H), "w_down": mat(H, I)}
+    for g in ("g1", "g2"):
+        w[g] = (torch.rand(H, generator=gen, device=device, dtype=torch.float32) + 0.5).to(
+            torch.bfloat16)
+    return w
+
+
+def block_input(batch: int, hidden: int, seed: int, device="cpu") -> torch.Tensor:
+    """The first block's input u, N(0, 1) bf16 [B, hidden]."""
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    return torch.randn(batch, hidden, generator=gen, device=device, dtype=torch.bfloat16)
