@@ -5,6 +5,11 @@ then qf_attn_combine (merge to bf16 out + fp32 lse).  All layers' inputs are res
 before the timed region.  Prints ONE JSON line.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+With ``--stage NAME`` it instead times a decode step of a stack of Q-First blocks (synthetic
+weights) at the context where the feed-forward's weight bytes equal the sweep's cache bytes, with
+the sweep in the serial order and on its own stream beside the feed-forward (both captured in HIP
+graphs), and prints one JSON line for that.
 """
 
 from __future__ import annotations
@@ -61,7 +66,7 @@ def committed_traffic(workload):
     with open(path) as f:
         rec = json.load(f)
     h = hashlib.sha256()
-    for name in ("decode_split.hip", "qf_internal.h"):
+    for name in ("decode_split.hip", "linear_body.h", "qf_internal.h"):
         with open(os.path.join(ROOT, "paper_2608_15473_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     if h.hexdigest() != rec.get("kernel_source_sha256"):
@@ -113,6 +118,85 @@ def cpu_baseline(cases, budget_s=15.0):
                       f"{len(os.sched_getaffinity(0))} usable cores"}
 
 
+def run_stage(args, dev):
+    """Decode steps of a stack of Q-First blocks in the three orders of the same launches (one
+    stream; the sweep on a second stream; the sweep and W_gate|W_up in one launch), each captured
+    in a HIP graph, plus the attention side alone.  Each replay appends one position per layer,
+    so the caches get room for every replay."""
+    import torch
+
+    from paper_2608_15473_amd.stage import MODES, LayerCache, QFirstStack
+    from workloads import (BLOCKS, SCALE, STAGE_WORKLOADS, block_input, block_weights,
+                           kv_bytes_per_position, make_case)
+
+    w = STAGE_WORKLOADS[args.stage]
+    shape = BLOCKS[w.block]
+    L = args.layers or shape.layers
+    K, W = args.steps, args.warmup
+    order = list(MODES) + ["sweep_only"] + list(MODES)   # each mode twice, best kept
+    room = 2 * len(MODES) * (K + W) + len(MODES) + 8
+    log(f"[stage] generating {L} block(s) of {w.name}")
+    layers, caches = [], []
+    for l in range(L):
+        layers.append(block_weights(shape, seed=1000 * w.index + l, device=dev))
+        c = make_case(w.batch, shape.n_q_heads, shape.n_kv_heads, w.ctx + room, w.shards,
+                      seed=1000 * w.index + 500 + l, device=dev)
+        c.ctx_lens -= room
+        caches.append(LayerCache(c.k_cache, c.v_cache, c.block_table, c.ctx_lens, c.n_shards))
+    stack = QFirstStack(layers, caches, shape.n_q_heads, shape.n_kv_heads, w.shards, SCALE)
+    u = block_input(w.batch, shape.hidden, seed=1000 * w.index + 999, device=dev)
+
+    side = torch.cuda.Stream()                  # warm the libraries up before capturing
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for mode in MODES:
+            stack.step(u, mode=mode)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graphs = {mode: stack.capture(u, mode=mode)[0] for mode in MODES}
+    sweep_graph = torch.cuda.CUDAGraph()        # the attention side alone, every layer
+    with torch.cuda.graph(sweep_graph):
+        for c in stack.caches:
+            stack._sweep(c)
+    graphs["sweep_only"] = sweep_graph
+
+    ms = {}
+    for name in order:
+        g = graphs[name]
+        for _ in range(W):
+            g.replay()
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(K):
+            g.replay()
+        t1.record()
+        torch.cuda.synchronize()
+        ms[name] = min(ms.get(name, float("inf")), t0.elapsed_time(t1) / K)
+        log(f"[stage] {name}: {t0.elapsed_time(t1) / K:.4f} ms/step")
+    if int(stack.status.item()) != 0:
+        raise RuntimeError("a cache ran out of room during the stage bench")
+    print(json.dumps({
+        "metric": "Q-First decode step, sweep beside the feed-forward (one shared launch)",
+        "value": round(w.batch / (ms["fused"] * 1e-3), 1), "unit": "tokens/s",
+        "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": round(ms["fused"], 4), "higher_is_better": True, "dtype": "bf16",
+        "data": "synthetic",
+        "serial_ms_per_step": round(ms["serial"], 4),
+        "streams_ms_per_step": round(ms["streams"], 4),
+        "fused_ms_per_step": round(ms["fused"], 4),
+        "sweep_only_ms_per_step": round(ms["sweep_only"], 4),
+        "speedup_vs_serial": round(ms["serial"] / ms["fused"], 4),
+        "sweep_hidden_frac": round((ms["serial"] - ms["fused"]) / ms["sweep_only"], 4),
+        "config": {"workload": w.name, "block": shape.name, "layers": L, "batch": w.batch,
+                   "context": w.ctx, "shards": w.shards, "hidden": shape.hidden,
+                   "inter": shape.inter, "n_q_heads": shape.n_q_heads,
+                   "n_kv_heads": shape.n_kv_heads, "ffn_bytes_per_layer": shape.ffn_bytes(),
+                   "kv_bytes_per_layer": w.batch * w.ctx * kv_bytes_per_position(shape.n_kv_heads),
+                   "graphs": True},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -122,6 +206,8 @@ def main():
     ap.add_argument("--layers", type=int, default=None,
                     help="resident layers (default: the workload's own count)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--stage", default=None,
+                    help="time the [MLP || Attn] decode stage of this block workload instead")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="instead of the bench: one plain device copy of this many MiB (the "
                          "known-size reference that scales the FETCH_SIZE / WRITE_SIZE counters)")
@@ -148,6 +234,9 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes": n, "read_bytes": n, "write_bytes": n}))
+        return
+    if args.stage:
+        run_stage(args, dev)
         return
     w = WORKLOADS[args.workload]
     L = args.layers or w.layers

@@ -183,6 +183,64 @@ int qf_schedule_simulate(int32_t n_requests, const double* arrival, const double
                          double max_wait, double* finish, double* sweep_start, double* sweep_end,
                          double* ffn_depart, double* ffn_return);
 
+/*
+ * The dense products of a decoder block at decode (§2 protocol: q_j = W_q N1(u_j); the
+ * feed-forward M(N2 u_j); k_j, v_j = W_k N1(z_j), W_v N1(z_j); and W_o), each fused with the
+ * normalisation or activation that feeds it and the residual add that follows it:
+ *   out[m, n] = sum_k W[n, k] * P(x)[m, k]  (+ residual[m, n]),   m < rows, n < n_out, k < k
+ *   QF_LINEAR_PLAIN     P(x) = x                                   x: bf16 [rows, k]
+ *   QF_LINEAR_RMS_NORM  P(x) = x / sqrt(mean_k x^2 + eps) * gain   x: bf16 [rows, k], gain [k]
+ *   QF_LINEAR_SWIGLU    P(x) = silu(x[:, :k]) * x[:, k:2k],  silu(t) = t / (1 + exp(-t))
+ *                                                                  x: bf16 [rows, 2k]
+ * (RMS normalisation and the SwiGLU feed-forward are the forms of the Qwen3 blocks the paper
+ * converts; the paper itself names only "a normalisation" and "the feed-forward".)
+ * W: bf16 [n_out, k] row-major (torch's [out, in] layout).  Outputs n < n_split go to
+ * out [rows, n_split], the rest to out_b [rows, n_out - n_split] (one product can fill k and v);
+ * residual: bf16 [rows, n_out] or NULL.  fp32 arithmetic, one round-to-nearest-even per output;
+ * out must not alias x or residual.  Device pointers, caller-owned; asynchronous on `stream`.
+ * Returns QF_OK; QF_EINVAL (rows < 0, n_out < 1, k < 8, unknown prologue, n_split outside
+ * [1, n_out], eps < 0 or NaN with RMS_NORM, NULL x / w / out, NULL gain with RMS_NORM, NULL out_b
+ * with n_split < n_out); QF_EUNSUPPORTED (rows > 8, k not a multiple of 8); QF_EALIGN (x, w, gain
+ * not 16-byte aligned, out, out_b, residual not 2-byte aligned); QF_EHIP (launch failed).
+ * rows == 0 is a no-op.
+ */
+#define QF_LINEAR_PLAIN 0
+#define QF_LINEAR_RMS_NORM 1
+#define QF_LINEAR_SWIGLU 2
+int qf_linear(int32_t rows, int32_t n_out, int32_t k, int32_t prologue, const void* x,
+              const void* w, const void* gain, float eps, const void* residual, void* out,
+              int32_t n_split, void* out_b, void* stream);
+
+/* The arguments of one qf_linear call, as a struct (for qf_attn_decode_split_beside). */
+typedef struct {
+  int32_t rows, n_out, k, prologue;
+  const void* x;
+  const void* w;
+  const void* gain;
+  float eps;
+  const void* residual;
+  void* out;
+  int32_t n_split;
+  void* out_b;
+} qf_linear_args;
+
+/*
+ * The sweep beside the feed-forward (§3, "across layers": neither is downstream of the other, so
+ * they may run at once): exactly qf_attn_decode_split(desc, q, ..., workspace_size) and
+ * qf_linear(*beside), issued as ONE launch whose workgroups take either role, so that on one GPU
+ * the two share every CU instead of running one after the other.  Results are bitwise those of
+ * the two separate calls.  The caller guarantees that neither call's outputs overlap the other's
+ * inputs or outputs.  Arguments, errors and ownership are those of the two calls (checked before
+ * anything is launched); `beside` is a host pointer, read during the call.  With batch == 0 or
+ * beside->rows == 0 only the other call is issued.
+ */
+int qf_attn_decode_split_beside(const qf_decode_desc* desc, const void* q, const void* k_cache,
+                                const void* v_cache, const int32_t* block_table,
+                                const int32_t* ctx_lens, const int32_t* n_shards,
+                                float* part_out, float* part_lse, void* workspace,
+                                size_t workspace_size, const qf_linear_args* beside,
+                                void* stream);
+
 /* Message for the last error on the calling thread; "" if none.  Valid until the thread's next
  * call into the library. */
 const char* qf_last_error(void);

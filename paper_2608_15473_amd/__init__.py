@@ -12,16 +12,22 @@ from .binding import (  # noqa: F401
     QF_EHIP,
     QF_EINVAL,
     QF_EUNSUPPORTED,
+    QF_LINEAR_PLAIN,
+    QF_LINEAR_RMS_NORM,
+    QF_LINEAR_SWIGLU,
     QF_OK,
     DecodeDesc,
+    LinearArgs,
     QFError,
     attn_combine,
     attn_combine_current,
     attn_decode,
     attn_decode_split,
+    attn_decode_split_beside,
     kv_append,
     load_library,
     schedule_simulate,
     make_desc,
+    linear,
     workspace_size,
 )

@@ -17,9 +17,10 @@ LIB_PATH = os.path.join(_HERE, "lib", "libqfattn.so")
 
 QF_OK, QF_EINVAL, QF_EUNSUPPORTED, QF_EALIGN, QF_EHIP = 0, -1, -2, -3, -4
 EXPORTED = ("qf_attn_decode_split_workspace_size", "qf_attn_decode_split", "qf_attn_combine",
-            "qf_attn_combine_current", "qf_kv_append", "qf_schedule_simulate", "qf_last_error",
-            "qf_version")
+            "qf_attn_combine_current", "qf_kv_append", "qf_linear", "qf_attn_decode_split_beside",
+            "qf_schedule_simulate", "qf_last_error", "qf_version")
 QF_WIRING_QFIRST, QF_WIRING_COMPOSED = 0, 1
+QF_LINEAR_PLAIN, QF_LINEAR_RMS_NORM, QF_LINEAR_SWIGLU = 0, 1, 2
 
 
 class QFError(RuntimeError):
@@ -34,6 +35,13 @@ class DecodeDesc(ctypes.Structure):
                 ("page_size", ctypes.c_int32), ("max_pages_per_seq", ctypes.c_int32),
                 ("num_pages", ctypes.c_int32), ("max_shards", ctypes.c_int32),
                 ("softmax_scale", ctypes.c_float)]
+
+
+class LinearArgs(ctypes.Structure):
+    _fields_ = [("rows", ctypes.c_int32), ("n_out", ctypes.c_int32), ("k", ctypes.c_int32),
+                ("prologue", ctypes.c_int32), ("x", ctypes.c_void_p), ("w", ctypes.c_void_p),
+                ("gain", ctypes.c_void_p), ("eps", ctypes.c_float), ("residual", ctypes.c_void_p),
+                ("out", ctypes.c_void_p), ("n_split", ctypes.c_int32), ("out_b", ctypes.c_void_p)]
 
 
 _lib = None
@@ -57,6 +65,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.qf_attn_combine_current.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, vp,
                                             ctypes.c_float, vp, vp, vp]
     lib.qf_kv_append.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp, vp, i32, vp, vp]
+    lib.qf_linear.argtypes = [i32, i32, i32, i32, vp, vp, vp, ctypes.c_float, vp, vp, i32, vp,
+                              vp]
+    lib.qf_attn_decode_split_beside.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp, vp,
+                                                vp, vp, vp, sz, ctypes.POINTER(LinearArgs), vp]
     dp = ctypes.POINTER(ctypes.c_double)
     lib.qf_schedule_simulate.argtypes = [i32, dp, dp, i32, i32, ctypes.c_double, i32,
                                          ctypes.c_double, dp, dp, dp, dp, dp]
@@ -65,7 +77,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.qf_version.argtypes = []
     for name in ("qf_attn_decode_split_workspace_size", "qf_attn_decode_split",
                  "qf_attn_combine", "qf_attn_combine_current", "qf_kv_append",
-                 "qf_schedule_simulate", "qf_version"):
+                 "qf_linear", "qf_attn_decode_split_beside", "qf_schedule_simulate", "qf_version"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -109,15 +121,9 @@ def workspace_size(desc: DecodeDesc) -> int:
     return n.value
 
 
-def attn_decode_split(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards=None,
-                      scale=None, part_out=None, part_lse=None, workspace=None,
-                      max_pages=None):
-    """The sweep split into position shards (qf_attn_decode_split).
-
-    q bf16 [B, Hq, D]; k_cache / v_cache bf16 [num_pages, Hkv, P, D]; block_table int32
-    [B, max_pages] or None (identity); ctx_lens int32 [B]; n_shards an int or int32 [B].
-    Returns (part_out fp32 [B, S_max, Hq, D], part_lse fp32 [B, S_max, Hq]).
-    """
+def _split_call(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards, scale,
+                part_out, part_lse, workspace, max_pages):
+    """Checks and allocations of qf_attn_decode_split: returns (C arguments, part_out, part_lse)."""
     _require(q, "q", torch.bfloat16, 3)
     _require(k_cache, "k_cache", torch.bfloat16, 4)
     _require(v_cache, "v_cache", torch.bfloat16, 4)
@@ -148,12 +154,46 @@ def attn_decode_split(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_
     if need and workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    args = (ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+            _ptr(ctx_lens), _ptr(n_shards), _ptr(part_out), _ptr(part_lse), _ptr(workspace),
+            ws_bytes)
+    return args, desc, part_out, part_lse
+
+
+def attn_decode_split(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards=None,
+                      scale=None, part_out=None, part_lse=None, workspace=None,
+                      max_pages=None):
+    """The sweep split into position shards (qf_attn_decode_split).
+
+    q bf16 [B, Hq, D]; k_cache / v_cache bf16 [num_pages, Hkv, P, D]; block_table int32
+    [B, max_pages] or None (identity); ctx_lens int32 [B]; n_shards an int or int32 [B].
+    Returns (part_out fp32 [B, S_max, Hq, D], part_lse fp32 [B, S_max, Hq]).
+    """
+    args, desc, part_out, part_lse = _split_call(q, k_cache, v_cache, block_table, ctx_lens,
+                                                 n_shards, max_shards, scale, part_out, part_lse,
+                                                 workspace, max_pages)
     stream = torch.cuda.current_stream(q.device).cuda_stream
-    _check(load_library().qf_attn_decode_split(
-        ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
-        _ptr(ctx_lens), _ptr(n_shards), _ptr(part_out), _ptr(part_lse), _ptr(workspace),
-        ws_bytes, ctypes.c_void_p(stream)))
+    _check(load_library().qf_attn_decode_split(*args, ctypes.c_void_p(stream)))
     return part_out, part_lse
+
+
+def attn_decode_split_beside(q, k_cache, v_cache, block_table, ctx_lens, n_shards, beside,
+                             max_shards=None, scale=None, part_out=None, part_lse=None,
+                             workspace=None, max_pages=None):
+    """The sweep and one fused product in a single launch (qf_attn_decode_split_beside).
+
+    The sweep's arguments are those of ``attn_decode_split``; ``beside`` is a dict of ``linear``'s
+    keyword arguments (x, w, prologue, gain, eps, residual, out, split, out_b).  Returns
+    (part_out, part_lse, the product's output(s)); bitwise the results of the two separate calls.
+    """
+    args, desc, part_out, part_lse = _split_call(q, k_cache, v_cache, block_table, ctx_lens,
+                                                 n_shards, max_shards, scale, part_out, part_lse,
+                                                 workspace, max_pages)
+    la, result = _linear_call(**beside)
+    stream = torch.cuda.current_stream(q.device).cuda_stream
+    _check(load_library().qf_attn_decode_split_beside(*args, ctypes.byref(la),
+                                                      ctypes.c_void_p(stream)))
+    return part_out, part_lse, result
 
 
 def attn_combine(part_out, part_lse, out=None, lse=None, want_lse=True):
@@ -221,6 +261,60 @@ def kv_append(k_cache, v_cache, block_table, ctx_lens, k_new, v_new, advance=Tru
                                        _ptr(block_table), _ptr(ctx_lens), _ptr(k_new),
                                        _ptr(v_new), 1 if advance else 0, _ptr(status),
                                        ctypes.c_void_p(stream)))
+
+
+_PROLOGUES = {None: QF_LINEAR_PLAIN, "rms_norm": QF_LINEAR_RMS_NORM, "swiglu": QF_LINEAR_SWIGLU}
+
+
+def _linear_call(x, w, prologue=None, gain=None, eps=1e-6, residual=None, out=None, split=None,
+                 out_b=None):
+    """Checks and allocations of qf_linear: returns (LinearArgs, the output(s))."""
+    if prologue not in _PROLOGUES:
+        raise QFError(QF_EINVAL, f"unknown prologue {prologue!r}")
+    _require(x, "x", torch.bfloat16, 2)
+    _require(w, "w", torch.bfloat16, 2)
+    M = x.shape[0]
+    N, K = w.shape
+    if x.shape[1] != (2 * K if prologue == "swiglu" else K):
+        raise QFError(QF_EINVAL, f"x has {x.shape[1]} columns for a weight of {K} inputs")
+    if gain is not None:
+        _require(gain, "gain", torch.bfloat16, 1)
+    if residual is not None:
+        _require(residual, "residual", torch.bfloat16, 2)
+        if tuple(residual.shape) != (M, N):
+            raise QFError(QF_EINVAL, "residual must be [M, N]")
+    n_split = N if split is None else int(split)
+    if out is None:
+        out = torch.empty((M, n_split), dtype=torch.bfloat16, device=x.device)
+    if n_split < N and out_b is None:
+        out_b = torch.empty((M, N - n_split), dtype=torch.bfloat16, device=x.device)
+    _require(out, "out", torch.bfloat16)
+    if out.numel() != M * n_split:
+        raise QFError(QF_EINVAL, "out must hold [M, split] elements")
+    if out_b is not None:
+        _require(out_b, "out_b", torch.bfloat16)
+        if out_b.numel() != M * (N - n_split):
+            raise QFError(QF_EINVAL, "out_b must hold [M, N - split] elements")
+    la = LinearArgs(M, N, K, _PROLOGUES[prologue], x.data_ptr(), w.data_ptr(),
+                    None if gain is None else gain.data_ptr(), float(eps),
+                    None if residual is None else residual.data_ptr(), out.data_ptr(), n_split,
+                    None if out_b is None else out_b.data_ptr())
+    return la, ((out, out_b) if n_split < N else out)
+
+
+def linear(x, w, prologue=None, gain=None, eps=1e-6, residual=None, out=None, split=None,
+           out_b=None):
+    """out = W . P(x) (+ residual) for up to 8 rows (qf_linear), all bf16.
+
+    x [M, K] ([M, 2K] for "swiglu": gate, then up); w [N, K] (torch layout); prologue None,
+    "rms_norm" (with ``gain`` [K]) or "swiglu".  With ``split`` the first ``split`` outputs go to
+    ``out`` [M, split] and the rest to ``out_b`` [M, N - split]."""
+    la, result = _linear_call(x, w, prologue, gain, eps, residual, out, split, out_b)
+    stream = torch.cuda.current_stream(x.device).cuda_stream
+    _check(load_library().qf_linear(la.rows, la.n_out, la.k, la.prologue, la.x, la.w, la.gain,
+                                    la.eps, la.residual, la.out, la.n_split, la.out_b,
+                                    ctypes.c_void_p(stream)))
+    return result
 
 
 def attn_decode(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards=None,

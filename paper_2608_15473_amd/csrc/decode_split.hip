@@ -20,6 +20,7 @@
 // exceeds it by more than kLazy), so the O rescale is rare after a shard's first pages.
 #include <math.h>
 
+#include "linear_body.h"
 #include "qf_internal.h"
 
 namespace qf {
@@ -61,15 +62,16 @@ __device__ __forceinline__ void unpack8(const uint4& w, float* f) {
   f[6] = bf16_lo(w.w); f[7] = bf16_hi(w.w);
 }
 
+// The sweep of one unit by one workgroup; `bid` plays the role of the workgroup index (it is the
+// index itself in decode_split_kernel, the sweep's share of the indices in a shared launch).
 template <int G, int W, int NBUF>
-__global__ void __launch_bounds__(64 * W)
-decode_split_kernel(const uint16_t* __restrict__ qp, const uint16_t* __restrict__ kp,
-                    const uint16_t* __restrict__ vp, const int32_t* __restrict__ block_table,
-                    const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ n_shards,
-                    float* __restrict__ out_o, float* __restrict__ out_lse, int32_t hq,
-                    int32_t hkv, int32_t max_pages, int32_t num_pages, int32_t max_shards,
-                    int32_t chunks, int32_t n_units, int32_t units_per_xcd, int32_t batch,
-                    int32_t order, float scale_log2) {
+__device__ __forceinline__ void sweep_unit(
+    const uint16_t* __restrict__ qp, const uint16_t* __restrict__ kp,
+    const uint16_t* __restrict__ vp, const int32_t* __restrict__ block_table,
+    const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ n_shards,
+    float* __restrict__ out_o, float* __restrict__ out_lse, int32_t hq, int32_t hkv,
+    int32_t max_pages, int32_t num_pages, int32_t max_shards, int32_t chunks, int32_t n_units,
+    int32_t units_per_xcd, int32_t batch, int32_t order, float scale_log2, const unsigned bid) {
   // Which unit this workgroup sweeps.  Workgroups are dispatched in index order, round-robin over
   // the 8 XCDs.
   //  * Short shards (kOrderByRequest): each XCD takes a contiguous range of units in (request,
@@ -80,7 +82,7 @@ decode_split_kernel(const uint16_t* __restrict__ qp, const uint16_t* __restrict_
   //    start first and every XCD gets an even share; the small shards fill the tail.
   int g, c, s, b;
   if (order == kOrderByRequest) {
-    const int unit = (int)(blockIdx.x % 8u) * units_per_xcd + (int)(blockIdx.x / 8u);
+    const int unit = (int)(bid % 8u) * units_per_xcd + (int)(bid / 8u);
     if (unit >= n_units) return;
     g = unit % hkv;
     int rest = unit / hkv;
@@ -89,7 +91,7 @@ decode_split_kernel(const uint16_t* __restrict__ qp, const uint16_t* __restrict_
     s = rest % max_shards;
     b = rest / max_shards;
   } else {
-    const int unit = (int)blockIdx.x;
+    const int unit = (int)bid;
     if (unit >= n_units) return;
     g = unit % hkv;
     int rest = unit / hkv;
@@ -320,6 +322,20 @@ swept:
   }
 }
 
+template <int G, int W, int NBUF>
+__global__ void __launch_bounds__(64 * W)
+decode_split_kernel(const uint16_t* __restrict__ qp, const uint16_t* __restrict__ kp,
+                    const uint16_t* __restrict__ vp, const int32_t* __restrict__ block_table,
+                    const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ n_shards,
+                    float* __restrict__ out_o, float* __restrict__ out_lse, int32_t hq,
+                    int32_t hkv, int32_t max_pages, int32_t num_pages, int32_t max_shards,
+                    int32_t chunks, int32_t n_units, int32_t units_per_xcd, int32_t batch,
+                    int32_t order, float scale_log2) {
+  sweep_unit<G, W, NBUF>(qp, kp, vp, block_table, ctx_lens, n_shards, out_o, out_lse, hq, hkv,
+                         max_pages, num_pages, max_shards, chunks, n_units, units_per_xcd, batch,
+                         order, scale_log2, blockIdx.x);
+}
+
 template <int G>
 hipError_t launch_g(const SplitParams& p, hipStream_t stream) {
   const unsigned grid = 8u * (unsigned)p.units_per_xcd;
@@ -330,6 +346,74 @@ hipError_t launch_g(const SplitParams& p, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// One launch, two roles: the sweep's workgroups and those of a fused product (linear_body.h) share
+// one grid, so the hardware dispatcher runs both at once on every CU (the sweep beside the
+// feed-forward, §3).  Groups of 8 consecutive workgroup indices (one per XCD) are dealt to the two
+// roles in proportion to their sizes, so both start together and each keeps its index modulo 8;
+// every workgroup does exactly what it would do in its own launch.
+// The occupancy the sweep alone reaches (registers), asked of the shared kernel too, so that
+// the product's role does not lower it.
+template <int G, int MB>
+__global__ void __launch_bounds__(64 * kSplitWaves)
+__attribute__((amdgpu_waves_per_eu(G >= 8 ? 2 : 3)))
+sweep_beside_linear_kernel(
+    const uint16_t* __restrict__ qp, const uint16_t* __restrict__ kp,
+    const uint16_t* __restrict__ vp, const int32_t* __restrict__ block_table,
+    const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ n_shards,
+    float* __restrict__ out_o, float* __restrict__ out_lse, int32_t hq, int32_t hkv,
+    int32_t max_pages, int32_t num_pages, int32_t max_shards, int32_t chunks, int32_t n_units,
+    int32_t units_per_xcd, int32_t batch, int32_t order, float scale_log2,
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
+    const uint16_t* __restrict__ gain, const uint16_t* __restrict__ residual,
+    uint16_t* __restrict__ out_a, uint16_t* __restrict__ out_b, int32_t M, int32_t N, int32_t K,
+    int32_t n_split, float eps, int32_t prologue, int32_t linear_groups) {
+  static_assert(64 * kSplitWaves == lin::kThreads, "both roles use the same workgroup size");
+  const unsigned j = blockIdx.x / 8u, lane8 = blockIdx.x % 8u;
+  const unsigned long long S = (unsigned)units_per_xcd, T = S + (unsigned)linear_groups;
+  const unsigned before = (unsigned)(j * S / T);          // sweep groups dealt before group j
+  if ((unsigned)((j + 1ull) * S / T) > before) {
+    sweep_unit<G, kSplitWaves, kSplitBuffers>(qp, kp, vp, block_table, ctx_lens, n_shards, out_o,
+                                              out_lse, hq, hkv, max_pages, num_pages, max_shards,
+                                              chunks, n_units, units_per_xcd, batch, order,
+                                              scale_log2, 8u * before + lane8);
+    return;
+  }
+  constexpr int U = 2, R = lin::beside_rows(MB);
+  const unsigned lb = 8u * (j - before) + lane8;
+  if (prologue == kProRmsNorm)
+    lin::linear_rows<kProRmsNorm, MB, U, R>(x, w, gain, residual, out_a, out_b, M, N, K, n_split,
+                                            eps, lb);
+  else if (prologue == kProSwiglu)
+    lin::linear_rows<kProSwiglu, MB, U, R>(x, w, gain, residual, out_a, out_b, M, N, K, n_split,
+                                           eps, lb);
+  else
+    lin::linear_rows<kProNone, MB, U, R>(x, w, gain, residual, out_a, out_b, M, N, K, n_split,
+                                         eps, lb);
+}
+
+template <int G, int MB>
+hipError_t launch_beside(const SplitParams& p, const LinearParams& l, hipStream_t stream) {
+  const int linear_groups = (lin::linear_blocks(l.N, lin::beside_rows(MB)) + 7) / 8;
+  const unsigned grid = 8u * ((unsigned)p.units_per_xcd + (unsigned)linear_groups);
+  hipLaunchKernelGGL((sweep_beside_linear_kernel<G, MB>), dim3(grid), dim3(64 * kSplitWaves), 0,
+                     stream, p.q, p.k, p.v, p.block_table, p.ctx_lens, p.n_shards, p.out_o,
+                     p.out_lse, p.hq, p.hkv, p.max_pages, p.num_pages, p.max_shards, p.chunks,
+                     p.n_units, p.units_per_xcd, p.batch, p.order, p.scale_log2, l.x, l.w, l.gain,
+                     l.residual, l.out_a, l.out_b, l.M, l.N, l.K, l.n_split, l.eps, l.prologue,
+                     linear_groups);
+  return hipGetLastError();
+}
+
+template <int G>
+hipError_t launch_beside_g(const SplitParams& p, const LinearParams& l, hipStream_t stream) {
+  switch (lin::rows_bucket(l.M)) {
+    case 1: return launch_beside<G, 1>(p, l, stream);
+    case 2: return launch_beside<G, 2>(p, l, stream);
+    case 4: return launch_beside<G, 4>(p, l, stream);
+    default: return launch_beside<G, 8>(p, l, stream);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_decode_split(const SplitParams& p, int group, hipStream_t stream) {
@@ -338,6 +422,17 @@ hipError_t launch_decode_split(const SplitParams& p, int group, hipStream_t stre
     case 2: return launch_g<2>(p, stream);
     case 4: return launch_g<4>(p, stream);
     case 8: return launch_g<8>(p, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_decode_split_beside(const SplitParams& p, int group, const LinearParams& l,
+                                     hipStream_t stream) {
+  switch (group) {
+    case 1: return launch_beside_g<1>(p, l, stream);
+    case 2: return launch_beside_g<2>(p, l, stream);
+    case 4: return launch_beside_g<4>(p, l, stream);
+    case 8: return launch_beside_g<8>(p, l, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -67,6 +67,23 @@ struct AppendParams {
 };
 
 hipError_t launch_kv_append(const AppendParams& p, hipStream_t stream);
+// out = W . P(x) (+ residual) for a few input rows (block_ops.hip).
+constexpr int kProNone = 0, kProRmsNorm = 1, kProSwiglu = 2;
+constexpr int kLinearMaxRows = 8;
+struct LinearParams {
+  const uint16_t* x;         // bf16 [M, K] ([M, 2K] for kProSwiglu: gate, then up)
+  const uint16_t* w;         // bf16 [N, K]
+  const uint16_t* gain;      // bf16 [K] (kProRmsNorm)
+  const uint16_t* residual;  // bf16 [M, N] or nullptr
+  uint16_t* out_a;           // bf16 [M, n_split]
+  uint16_t* out_b;           // bf16 [M, N - n_split]
+  int M, N, K, n_split, prologue;
+  float eps;
+};
+hipError_t launch_linear(const LinearParams& p, hipStream_t stream);
+// The sweep and a fused product in one launch (decode_split.hip).
+hipError_t launch_decode_split_beside(const SplitParams& p, int group, const LinearParams& l,
+                                      hipStream_t stream);
 
 // Host simulation of the layer-wise decode schedule (schedule.cpp).
 int simulate_schedule(int R, const double* arrival, const double* attn_time, int L, int wiring,

@@ -68,32 +68,26 @@ size_t workspace_bytes(const qf_decode_desc* d, int64_t chunks) {
   return states * qf::kHeadDim * sizeof(float) + states * sizeof(float);
 }
 
-}  // namespace
+// Everything qf_attn_decode_split checks and derives before launching.
+struct Split {
+  bool noop = false;
+  int group = 1;
+  int64_t chunks = 1;
+  qf::SplitParams p{};
+  qf::MergeParams chunk_merge{};
+};
 
-extern "C" {
-
-int qf_version(void) { return QF_VERSION; }
-
-const char* qf_last_error(void) { return g_error; }
-
-int qf_attn_decode_split_workspace_size(const qf_decode_desc* desc, size_t* bytes) {
-  g_error[0] = 0;
-  const int rc = check_desc(desc);
-  if (rc) return rc;
-  if (!bytes) return fail(QF_EINVAL, "bytes is NULL");
-  *bytes = workspace_bytes(desc, choose_chunks(desc));
-  return QF_OK;
-}
-
-int qf_attn_decode_split(const qf_decode_desc* desc, const void* q, const void* k_cache,
-                         const void* v_cache, const int32_t* block_table,
-                         const int32_t* ctx_lens, const int32_t* n_shards, float* part_out,
-                         float* part_lse, void* workspace, size_t workspace_size, void* stream) {
-  g_error[0] = 0;
+int prepare_split(const qf_decode_desc* desc, const void* q, const void* k_cache,
+                  const void* v_cache, const int32_t* block_table, const int32_t* ctx_lens,
+                  const int32_t* n_shards, float* part_out, float* part_lse, void* workspace,
+                  size_t workspace_size, Split* sp) {
   int rc = check_desc(desc);
   if (rc) return rc;
   const qf_decode_desc& d = *desc;
-  if (d.batch == 0) return QF_OK;
+  if (d.batch == 0) {
+    sp->noop = true;
+    return QF_OK;
+  }
   if (!q || !k_cache || !v_cache || !ctx_lens || !n_shards || !part_out || !part_lse)
     return fail(QF_EINVAL, "a required pointer is NULL");
   if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(part_out, 16))
@@ -146,11 +140,11 @@ int qf_attn_decode_split(const qf_decode_desc* desc, const void* q, const void* 
   p.order = shard_pages >= qf::kLongShardPages ? qf::kOrderByShardDesc : qf::kOrderByRequest;
   p.scale_log2 = (float)((double)d.softmax_scale * 1.4426950408889634);
 
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e = qf::launch_decode_split(p, d.n_q_heads / d.n_kv_heads, s);
-  if (e != hipSuccess) return fail(QF_EHIP, "decode_split launch: %s", hipGetErrorString(e));
+  sp->group = d.n_q_heads / d.n_kv_heads;
+  sp->chunks = chunks;
+  sp->p = p;
   if (chunks > 1) {
-    qf::MergeParams m{};
+    qf::MergeParams& m = sp->chunk_merge;
     m.in_o = p.out_o;
     m.in_lse = p.out_lse;
     m.out_o = part_out;
@@ -158,10 +152,95 @@ int qf_attn_decode_split(const qf_decode_desc* desc, const void* q, const void* 
     m.rows = d.batch * d.max_shards;
     m.entries = (int32_t)chunks;
     m.hq = d.n_q_heads;
-    e = qf::launch_merge(m, false, s);
-    if (e != hipSuccess) return fail(QF_EHIP, "chunk merge launch: %s", hipGetErrorString(e));
   }
   return QF_OK;
+}
+
+// After the sweep's launch: fold the chunks of each shard into the caller's per-shard partials.
+int finish_split(const Split& sp, hipStream_t s) {
+  if (sp.chunks <= 1) return QF_OK;
+  const hipError_t e = qf::launch_merge(sp.chunk_merge, false, s);
+  if (e != hipSuccess) return fail(QF_EHIP, "chunk merge launch: %s", hipGetErrorString(e));
+  return QF_OK;
+}
+
+// Everything qf_linear checks and derives before launching.
+int prepare_linear(const qf_linear_args* a, qf::LinearParams* out_p, bool* noop) {
+  const int32_t rows = a->rows, n_out = a->n_out, k = a->k, prologue = a->prologue;
+  const int32_t n_split = a->n_split;
+  const void *x = a->x, *w = a->w, *gain = a->gain, *residual = a->residual;
+  void *out = a->out, *out_b = a->out_b;
+  const float eps = a->eps;
+  if (rows < 0) return fail(QF_EINVAL, "rows must be >= 0 (got %d)", rows);
+  if (rows > qf::kLinearMaxRows)
+    return fail(QF_EUNSUPPORTED, "at most %d rows per call (got %d)", qf::kLinearMaxRows, rows);
+  if (n_out < 1 || k < 8) return fail(QF_EINVAL, "need n_out >= 1 and k >= 8");
+  if (k % 8) return fail(QF_EUNSUPPORTED, "k must be a multiple of 8 (got %d)", k);
+  if (prologue != QF_LINEAR_PLAIN && prologue != QF_LINEAR_RMS_NORM &&
+      prologue != QF_LINEAR_SWIGLU)
+    return fail(QF_EINVAL, "unknown prologue %d", prologue);
+  if (n_split < 1 || n_split > n_out)
+    return fail(QF_EINVAL, "n_split must be in [1, n_out] (got %d)", n_split);
+  if (prologue == QF_LINEAR_RMS_NORM && !(eps >= 0.0f)) return fail(QF_EINVAL, "eps must be >= 0");
+  if (rows == 0) {
+    *noop = true;
+    return QF_OK;
+  }
+  if (!x || !w || !out || (prologue == QF_LINEAR_RMS_NORM && !gain) ||
+      (n_split < n_out && !out_b))
+    return fail(QF_EINVAL, "a required pointer is NULL");
+  if (!aligned(x, 16) || !aligned(w, 16) || (gain && !aligned(gain, 16)) ||
+      !aligned(out, 2) || (out_b && !aligned(out_b, 2)) || (residual && !aligned(residual, 2)))
+    return fail(QF_EALIGN, "x, w and gain must be 16-byte aligned, out and residual 2-byte");
+  qf::LinearParams p{};
+  p.x = static_cast<const uint16_t*>(x);
+  p.w = static_cast<const uint16_t*>(w);
+  p.gain = static_cast<const uint16_t*>(gain);
+  p.residual = static_cast<const uint16_t*>(residual);
+  p.out_a = static_cast<uint16_t*>(out);
+  p.out_b = static_cast<uint16_t*>(out_b);
+  p.M = rows;
+  p.N = n_out;
+  p.K = k;
+  p.n_split = n_split;
+  p.prologue = prologue == QF_LINEAR_RMS_NORM ? qf::kProRmsNorm
+             : prologue == QF_LINEAR_SWIGLU   ? qf::kProSwiglu
+                                              : qf::kProNone;
+  p.eps = eps;
+  *out_p = p;
+  return QF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int qf_version(void) { return QF_VERSION; }
+
+const char* qf_last_error(void) { return g_error; }
+
+int qf_attn_decode_split_workspace_size(const qf_decode_desc* desc, size_t* bytes) {
+  g_error[0] = 0;
+  const int rc = check_desc(desc);
+  if (rc) return rc;
+  if (!bytes) return fail(QF_EINVAL, "bytes is NULL");
+  *bytes = workspace_bytes(desc, choose_chunks(desc));
+  return QF_OK;
+}
+
+int qf_attn_decode_split(const qf_decode_desc* desc, const void* q, const void* k_cache,
+                         const void* v_cache, const int32_t* block_table,
+                         const int32_t* ctx_lens, const int32_t* n_shards, float* part_out,
+                         float* part_lse, void* workspace, size_t workspace_size, void* stream) {
+  g_error[0] = 0;
+  Split sp;
+  const int rc = prepare_split(desc, q, k_cache, v_cache, block_table, ctx_lens, n_shards,
+                               part_out, part_lse, workspace, workspace_size, &sp);
+  if (rc || sp.noop) return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const hipError_t e = qf::launch_decode_split(sp.p, sp.group, s);
+  if (e != hipSuccess) return fail(QF_EHIP, "decode_split launch: %s", hipGetErrorString(e));
+  return finish_split(sp, s);
 }
 
 int qf_attn_combine(int32_t batch, int32_t n_q_heads, int32_t head_dim, int32_t max_shards,
@@ -262,6 +341,49 @@ int qf_kv_append(const qf_decode_desc* desc, void* k_cache, void* v_cache,
   const hipError_t e = qf::launch_kv_append(p, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(QF_EHIP, "kv_append launch: %s", hipGetErrorString(e));
   return QF_OK;
+}
+
+int qf_linear(int32_t rows, int32_t n_out, int32_t k, int32_t prologue, const void* x,
+              const void* w, const void* gain, float eps, const void* residual, void* out,
+              int32_t n_split, void* out_b, void* stream) {
+  g_error[0] = 0;
+  const qf_linear_args a{rows, n_out, k, prologue, x, w, gain, eps, residual, out, n_split, out_b};
+  qf::LinearParams p{};
+  bool noop = false;
+  const int rc = prepare_linear(&a, &p, &noop);
+  if (rc || noop) return rc;
+  const hipError_t e = qf::launch_linear(p, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(QF_EHIP, "linear launch: %s", hipGetErrorString(e));
+  return QF_OK;
+}
+
+int qf_attn_decode_split_beside(const qf_decode_desc* desc, const void* q, const void* k_cache,
+                                const void* v_cache, const int32_t* block_table,
+                                const int32_t* ctx_lens, const int32_t* n_shards,
+                                float* part_out, float* part_lse, void* workspace,
+                                size_t workspace_size, const qf_linear_args* beside,
+                                void* stream) {
+  g_error[0] = 0;
+  if (!beside) return fail(QF_EINVAL, "beside is NULL");
+  Split sp;
+  int rc = prepare_split(desc, q, k_cache, v_cache, block_table, ctx_lens, n_shards, part_out,
+                         part_lse, workspace, workspace_size, &sp);
+  if (rc) return rc;
+  qf::LinearParams lp{};
+  bool lin_noop = false;
+  rc = prepare_linear(beside, &lp, &lin_noop);
+  if (rc) return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipSuccess;
+  if (sp.noop && lin_noop) return QF_OK;
+  if (sp.noop)
+    e = qf::launch_linear(lp, s);
+  else if (lin_noop)
+    e = qf::launch_decode_split(sp.p, sp.group, s);
+  else
+    e = qf::launch_decode_split_beside(sp.p, sp.group, lp, s);
+  if (e != hipSuccess) return fail(QF_EHIP, "decode_split_beside launch: %s", hipGetErrorString(e));
+  return sp.noop ? QF_OK : finish_split(sp, s);
 }
 
 int qf_schedule_simulate(int32_t n_requests, const double* arrival, const double* attn_time,

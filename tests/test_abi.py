@@ -144,6 +144,49 @@ def test_current_token_entry_points_reject_bad_arguments():
     assert g(ctypes.byref(_desc(batch=0)), None, None, None, None, None, None, 1, None, None) == 0
 
 
+def test_linear_rejects_bad_arguments():
+    lib = load_library()
+    a = ctypes.c_void_p(4096)
+    f = lib.qf_linear
+    P, R, S = qf.QF_LINEAR_PLAIN, qf.QF_LINEAR_RMS_NORM, qf.QF_LINEAR_SWIGLU
+    assert f(-1, 64, 64, P, a, a, None, 0.0, None, a, 64, None, None) == qf.QF_EINVAL
+    assert f(9, 64, 64, P, a, a, None, 0.0, None, a, 64, None, None) == qf.QF_EUNSUPPORTED
+    assert f(2, 0, 64, P, a, a, None, 0.0, None, a, 1, None, None) == qf.QF_EINVAL
+    assert f(2, 64, 4, P, a, a, None, 0.0, None, a, 64, None, None) == qf.QF_EINVAL
+    assert f(2, 64, 60, P, a, a, None, 0.0, None, a, 64, None, None) == qf.QF_EUNSUPPORTED
+    assert f(2, 64, 64, 7, a, a, None, 0.0, None, a, 64, None, None) == qf.QF_EINVAL
+    assert f(2, 64, 64, P, a, a, None, 0.0, None, a, 0, None, None) == qf.QF_EINVAL
+    assert f(2, 64, 64, P, a, a, None, 0.0, None, a, 65, None, None) == qf.QF_EINVAL
+    assert f(2, 64, 64, R, a, a, a, -1.0, None, a, 64, None, None) == qf.QF_EINVAL
+    assert f(2, 64, 64, R, a, a, a, float("nan"), None, a, 64, None, None) == qf.QF_EINVAL
+    assert f(2, 64, 64, R, a, a, None, 1e-6, None, a, 64, None, None) == qf.QF_EINVAL
+    assert f(2, 64, 64, P, a, a, None, 0.0, None, a, 32, None, None) == qf.QF_EINVAL
+    assert f(2, 64, 64, P, None, a, None, 0.0, None, a, 64, None, None) == qf.QF_EINVAL
+    assert f(2, 64, 64, S, a, ctypes.c_void_p(4104), None, 0.0, None, a, 64, None,
+             None) == qf.QF_EALIGN
+    assert f(2, 64, 64, P, a, a, None, 0.0, ctypes.c_void_p(4097), a, 64, None,
+             None) == qf.QF_EALIGN
+    assert f(0, 64, 64, P, None, None, None, 0.0, None, None, 64, None, None) == qf.QF_OK
+
+
+def test_beside_checks_both_calls_before_launching():
+    lib = load_library()
+    a = ctypes.c_void_p(4096)
+    d = _desc()
+    la = qf.LinearArgs(2, 64, 64, qf.QF_LINEAR_PLAIN, 4096, 4096, None, 0.0, None, 4096, 64, None)
+    f = lib.qf_attn_decode_split_beside
+    args = (a, a, a, a, a, a, a, a, a, 1 << 40)
+    assert f(ctypes.byref(d), *args, None, None) == qf.QF_EINVAL
+    assert f(ctypes.byref(_desc(head_dim=64)), *args, ctypes.byref(la), None) == qf.QF_EUNSUPPORTED
+    bad = qf.LinearArgs(9, 64, 64, qf.QF_LINEAR_PLAIN, 4096, 4096, None, 0.0, None, 4096, 64, None)
+    assert f(ctypes.byref(d), *args, ctypes.byref(bad), None) == qf.QF_EUNSUPPORTED
+    nul = qf.LinearArgs(2, 64, 64, qf.QF_LINEAR_PLAIN, None, 4096, None, 0.0, None, 4096, 64, None)
+    assert f(ctypes.byref(d), *args, ctypes.byref(nul), None) == qf.QF_EINVAL
+    none = qf.LinearArgs(0, 64, 64, qf.QF_LINEAR_PLAIN, None, None, None, 0.0, None, None, 64, None)
+    assert f(ctypes.byref(_desc(batch=0)), None, None, None, None, None, None, None, None, None, 0,
+             ctypes.byref(none), None) == qf.QF_OK
+
+
 def test_empty_batch_is_a_no_op():
     lib = load_library()
     d = _desc(batch=0)
