@@ -25,6 +25,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, 8 TB/s
+INFINITY_CACHE_BYTES = 256 << 20  # MI355X last-level (Infinity) cache
 DEFAULT_WORKLOAD = "qwen3-0.6b_b32_n32768_s64_l28"
 
 
@@ -85,34 +86,40 @@ def cpu_baseline(cases, budget_s=15.0):
     import oracle
 
     B, Hq, Hkv, D = cases[0].shape
-    done_bytes, spent, reqs, layers = 0, 0.0, 0, 0
-    for case in cases:
-        layers += 1
-        ctx = case.ctx_lens.cpu().numpy()
-        S = case.n_shards.cpu().numpy()
-        bt = case.block_table.cpu().numpy()
-        q = case.q.double().cpu().numpy()
-        for b in np.argsort(ctx)[::-1]:
-            npg = -(-int(ctx[b]) // 16)
-            idx = torch.as_tensor(bt[b, :npg], dtype=torch.long, device=case.k_cache.device)
-            k = case.k_cache.index_select(0, idx).float().cpu().numpy()
-            v = case.v_cache.index_select(0, idx).float().cpu().numpy()
-            table = np.arange(npg)[None, :]
-            t0 = time.perf_counter()
-            po, pl = oracle.decode_split(q[b:b + 1], k, v, table, ctx[b:b + 1], S[b:b + 1],
-                                         case.scale, int(S[b]))
-            oracle.fold_combine(po, pl)
-            spent += time.perf_counter() - t0
-            done_bytes += int(ctx[b]) * 2 * Hkv * D * 2
-            reqs += 1
+    done_bytes, spent, reqs, layers, passes = 0, 0.0, 0, 0, 0
+    while spent < budget_s:         # a workload smaller than the budget is timed again
+        before = spent
+        passes += 1
+        for case in cases:
+            layers += passes == 1
+            ctx = case.ctx_lens.cpu().numpy()
+            S = case.n_shards.cpu().numpy()
+            bt = case.block_table.cpu().numpy()
+            q = case.q.double().cpu().numpy()
+            for b in np.argsort(ctx)[::-1]:
+                npg = -(-int(ctx[b]) // 16)
+                idx = torch.as_tensor(bt[b, :npg], dtype=torch.long, device=case.k_cache.device)
+                k = case.k_cache.index_select(0, idx).float().cpu().numpy()
+                v = case.v_cache.index_select(0, idx).float().cpu().numpy()
+                table = np.arange(npg)[None, :]
+                t0 = time.perf_counter()
+                po, pl = oracle.decode_split(q[b:b + 1], k, v, table, ctx[b:b + 1], S[b:b + 1],
+                                             case.scale, int(S[b]))
+                oracle.fold_combine(po, pl)
+                spent += time.perf_counter() - t0
+                done_bytes += int(ctx[b]) * 2 * Hkv * D * 2
+                reqs += 1
+                if spent >= budget_s:
+                    break
             if spent >= budget_s:
                 break
-        if spent >= budget_s:
+        if spent == before:
             break
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    return {"value": done_bytes / spent / 1e9, "unit": "GB/s", "cores": int(threads),
+    return {"value": done_bytes / max(spent, 1e-9) / 1e9, "unit": "GB/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"{reqs} whole request(s) from the first {layers} layer(s) "
+            "sample": f"{reqs} whole request(s) from the first {layers} layer(s) in {passes} "
+                      f"pass(es) "
                       f"({done_bytes / 1e6:.0f} MB of KV, all "
                       f"{Hq} heads, per-shard partials + pairwise merge), {spent:.1f} s; host has "
                       f"{len(os.sched_getaffinity(0))} usable cores"}
@@ -240,9 +247,13 @@ def main():
         return
     w = WORKLOADS[args.workload]
     L = args.layers or w.layers
-    log(f"[bench] generating {L} layer(s) of {w.name} on {torch.cuda.get_device_name(0)}")
+    # Cold reads only: a workload whose layers fit the Infinity Cache twice over gets that many
+    # distinct resident copies, and each step reads the next L of them in turn.
+    first = workload_case(w.name, layer=0, device=dev)
+    copies = max(L, -(-2 * INFINITY_CACHE_BYTES // max(1, first.kv_bytes())))
+    log(f"[bench] generating {copies} layer(s) of {w.name} on {torch.cuda.get_device_name(0)}")
     t0 = time.time()
-    cases = [workload_case(w.name, layer=l, device=dev) for l in range(L)]
+    cases = [first] + [workload_case(w.name, layer=l, device=dev) for l in range(1, copies)]
     torch.cuda.synchronize()
     log(f"[bench] inputs resident in {time.time() - t0:.1f} s")
     B, Hq, Hkv, D = cases[0].shape
@@ -257,8 +268,13 @@ def main():
     need = qf.workspace_size(desc)
     ws = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
 
+    turn = [0]
+
     def step(events=None):
-        for l, c in enumerate(cases):
+        base = turn[0]
+        turn[0] += L
+        for l in range(L):
+            c = cases[(base + l) % copies]
             if events is not None:
                 events[l][0].record()
             qf.attn_decode_split(c.q, c.k_cache, c.v_cache, c.block_table, c.ctx_lens,
@@ -285,6 +301,7 @@ def main():
     sweep_avg_s = sum(sweep_ms) / len(sweep_ms) / 1e3
     log(f"[bench] {ms_per_step:.3f} ms/step, sweep launch avg {sweep_avg_s * 1e6:.1f} us")
 
+    ab = ab[:L]                     # every copy has the same lengths, so the same bytes
     kv_step = sum(a["kv"] for a in ab)
     value = kv_step / (ms_per_step / 1e3) / 1e9
     attended = sum(a["attended"] for a in ab) / L
@@ -306,7 +323,8 @@ def main():
         "config": {"workload": w.name, "batch": B, "n_q_heads": Hq, "n_kv_heads": Hkv,
                    "head_dim": D, "page": 16, "layers": L, "max_shards": S,
                    "context": w.ctx if w.ctx else "ragged", "kv_dtype": "bf16",
-                   "kv_bytes_per_step": kv_step, "workspace_bytes": need},
+                   "kv_bytes_per_step": kv_step, "workspace_bytes": need,
+                   "resident_layer_copies": copies},
         "hbm_peak_frac": round(value / HBM_PEAK_GBS, 4),
         "attended_tokens_per_s_per_layer": round(attended / (ms_per_step / 1e3 / L), 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
@@ -317,7 +335,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("[bench] cpu_baseline: timing the fp64 oracle on a bounded sample")
-        result["cpu_baseline"] = cpu_baseline(cases)
+        result["cpu_baseline"] = cpu_baseline(cases[:L])
     print(json.dumps(result), flush=True)
 
 

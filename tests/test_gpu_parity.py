@@ -202,3 +202,22 @@ def test_full_size_workload_layer(gpu, name):
         assert np.all(got["lse"] > 88.0)
     del case
     torch.cuda.empty_cache()
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", ["qwen3-0.6b_b32_n32768_s64_l28", "qwen3-4b_b16_n36480_s32_l36",
+                                  "qwen3-0.6b_b1_n1m_s16_l28_planted"])
+def test_full_size_every_layer_sampled(gpu, name):
+    """Every layer of the multi-layer workloads, at its real shape: one (request, head) per layer,
+    rotating through the batch and the heads."""
+    w = WORKLOADS[name]
+    for layer in range(w.layers):
+        case = workload_case(name, layer=layer, device=gpu)
+        B, Hq = case.shape[0], case.shape[1]
+        pair = ((7 * layer + 3) % B, (5 * layer + 1) % Hq)
+        got, _ = _run(case, f"{name} layer {layer}", [pair])
+        if w.planted:
+            assert np.all(np.isfinite(got["out"])) and np.all(got["lse"] > 88.0)
+        del case, got
+        torch.cuda.empty_cache()
+
