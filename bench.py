@@ -26,6 +26,8 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, 8 TB/s
 INFINITY_CACHE_BYTES = 256 << 20  # MI355X last-level (Infinity) cache
+WARMUP_SECONDS = 0.3              # default warm-up: the first tens of ms of a run are slower
+TIMED_SECONDS = 0.25              # default timed work
 DEFAULT_WORKLOAD = "qwen3-0.6b_b32_n32768_s64_l28"
 
 
@@ -139,7 +141,8 @@ def run_stage(args, dev):
     w = STAGE_WORKLOADS[args.stage]
     shape = BLOCKS[w.block]
     L = args.layers or shape.layers
-    K, W = args.steps, args.warmup
+    K = args.steps if args.steps is not None else 10
+    W = args.warmup if args.warmup is not None else 3
     order = list(MODES) + ["sweep_only"] + list(MODES)   # each mode twice, best kept
     room = 2 * len(MODES) * (K + W) + len(MODES) + 8
     log(f"[stage] generating {L} block(s) of {w.name}")
@@ -207,8 +210,11 @@ def run_stage(args, dev):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default: at least 10 and at least 0.25 s of work)")
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed steps first (default: at least 3 and at least 0.3 s; short "
+                         "runs measure a slower cold phase of the GPU)")
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--layers", type=int, default=None,
                     help="resident layers (default: the workload's own count)")
@@ -284,10 +290,19 @@ def main():
                 events[l][1].record()
             qf.attn_combine(po, pl, out=out, lse=lse)
 
-    for _ in range(args.warmup):
+    warm, t_w = 0, time.perf_counter()
+    while (warm < args.warmup) if args.warmup is not None else \
+            (warm < 3 or time.perf_counter() - t_w < WARMUP_SECONDS):
         step()
+        warm += 1
+        if args.warmup is None:
+            torch.cuda.synchronize()
     torch.cuda.synchronize()
-    log(f"[bench] warmup done; timing {args.steps} steps")
+    per_step = (time.perf_counter() - t_w) / max(1, warm)
+    if args.steps is None:
+        args.steps = max(10, int(TIMED_SECONDS / max(per_step, 1e-6)) + 1)
+    args.warmup = warm
+    log(f"[bench] warmup done ({warm} steps); timing {args.steps} steps")
     ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(L)]
           for _ in range(args.steps)]
     torch.cuda.synchronize()

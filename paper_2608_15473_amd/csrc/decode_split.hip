@@ -121,6 +121,17 @@ __device__ __forceinline__ void sweep_unit(
   const int c0 = p0 + (int)min((int64_t)c * cper, (int64_t)len);
   const int c1 = p0 + (int)min((int64_t)(c + 1) * cper, (int64_t)len);
 
+  // An empty unit (a slot past the request's shards, or an empty shard or chunk) reads nothing:
+  // its ln Z is -inf (NaN if the request's shape was out of range), its O is never read, so it
+  // stops here, before the query loads and the merge.  (Ragged batches are mostly such units.)
+  if (c0 >= c1) {
+    if (threadIdx.x < G) {
+      const size_t slot = (((size_t)b * max_shards + s) * chunks + c) * hq + (size_t)g * G;
+      __builtin_nontemporal_store(poison ? NAN : -INFINITY, &out_lse[slot + threadIdx.x]);
+    }
+    return;
+  }
+
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int row = lane >> 4;

@@ -137,6 +137,12 @@ def test_out_of_range_device_values_poison_lse(gpu):
     bad_s = make_case(2, 16, 8, [300, 300], [2, 99], seed=171, max_shards=4, device=gpu)
     g2 = run_gpu(bad_s)
     assert np.all(np.isnan(g2["lse"][1])) and np.all(np.isfinite(g2["lse"][0]))
+    neg = make_case(2, 16, 8, [300, 40], [1, 1], seed=172, max_shards=3, device=gpu)
+    neg.ctx_lens[1] = -5                       # out of range with nothing to read: empty units
+    g3 = run_gpu(neg)
+    assert np.all(np.isnan(g3["part_lse"][1]))                 # every slot of it, empty ones too
+    assert np.all(np.isnan(g3["lse"][1])) and np.all(np.isfinite(g3["lse"][0]))
+    assert np.all(g3["part_lse"][0, 1:] == -np.inf)            # a valid request's unused slots
 
 
 def test_empty_batch(gpu):
