@@ -12,9 +12,17 @@
  * and the pairs of all shards merge into the result of one sweep over the whole cache (§5: any
  * partition, any order; an empty shard is ln Z = -inf with a vector that is never read).
  *
+ * Entry points: the sweep and its merge (qf_attn_decode_split, qf_attn_combine); the decode step
+ * around them (qf_attn_combine_current folds in the current token, qf_kv_append writes it to the
+ * cache); the dense products of a decoder block (qf_linear) and the sweep sharing one launch with
+ * one of them (qf_attn_decode_split_beside); and a host-side simulation of the layer-wise decode
+ * schedule (qf_schedule_simulate).
+ *
  * Conventions shared by every entry point
- *   - Every pointer argument except `stream` is a DEVICE pointer, owned by the caller.  The library
- *     allocates no memory, keeps no pointer after returning and holds no per-call state.
+ *   - Every pointer argument except `stream` is a DEVICE pointer, owned by the caller, except
+ *     where a declaration says HOST (qf_schedule_simulate, the `beside` struct of
+ *     qf_attn_decode_split_beside).  The library allocates no memory, keeps no pointer after
+ *     returning and holds no per-call state.
  *   - Every call is asynchronous: it validates its arguments on the host, enqueues its kernels on
  *     `stream` (a hipStream_t; NULL = the legacy default stream) and returns without waiting.
  *   - Return value: QF_OK (0) or a negative QF_E* code.  On error nothing has been enqueued, and
@@ -36,7 +44,7 @@
 extern "C" {
 #endif
 
-#define QF_VERSION 1
+#define QF_VERSION 2
 
 #define QF_OK 0
 #define QF_EINVAL (-1)       /* null pointer, negative or inconsistent size, Hq % Hkv != 0   */
@@ -187,13 +195,13 @@ int qf_schedule_simulate(int32_t n_requests, const double* arrival, const double
  * The dense products of a decoder block at decode (§2 protocol: q_j = W_q N1(u_j); the
  * feed-forward M(N2 u_j); k_j, v_j = W_k N1(z_j), W_v N1(z_j); and W_o), each fused with the
  * normalisation or activation that feeds it and the residual add that follows it:
- *   out[m, n] = sum_k W[n, k] * P(x)[m, k]  (+ residual[m, n]),   m < rows, n < n_out, k < k
+ *   out[m, n] = sum_{i < k} W[n, i] * P(x)[m, i]  (+ residual[m, n]),   m < rows, n < n_out
  *   QF_LINEAR_PLAIN     P(x) = x                                   x: bf16 [rows, k]
- *   QF_LINEAR_RMS_NORM  P(x) = x / sqrt(mean_k x^2 + eps) * gain   x: bf16 [rows, k], gain [k]
+ *   QF_LINEAR_RMS_NORM  P(x) = x / sqrt(mean_i x^2 + eps) * gain   x: bf16 [rows, k], gain [k]
  *   QF_LINEAR_SWIGLU    P(x) = silu(x[:, :k]) * x[:, k:2k],  silu(t) = t / (1 + exp(-t))
  *                                                                  x: bf16 [rows, 2k]
- * (RMS normalisation and the SwiGLU feed-forward are the forms of the Qwen3 blocks the paper
- * converts; the paper itself names only "a normalisation" and "the feed-forward".)
+ * (The paper names N1, N2 only as normalisations and M only as the feed-forward; the RMS form and
+ * the SwiGLU feed-forward are those of the Qwen3 blocks it converts.)
  * W: bf16 [n_out, k] row-major (torch's [out, in] layout).  Outputs n < n_split go to
  * out [rows, n_split], the rest to out_b [rows, n_out - n_split] (one product can fill k and v);
  * residual: bf16 [rows, n_out] or NULL.  fp32 arithmetic, one round-to-nearest-even per output;
@@ -231,7 +239,7 @@ typedef struct {
  * the two share every CU instead of running one after the other.  Results are bitwise those of
  * the two separate calls.  The caller guarantees that neither call's outputs overlap the other's
  * inputs or outputs.  Arguments, errors and ownership are those of the two calls (checked before
- * anything is launched); `beside` is a host pointer, read during the call.  With batch == 0 or
+ * anything is launched); `beside` is a HOST pointer, read during the call.  With batch == 0 or
  * beside->rows == 0 only the other call is issued.
  */
 int qf_attn_decode_split_beside(const qf_decode_desc* desc, const void* q, const void* k_cache,
