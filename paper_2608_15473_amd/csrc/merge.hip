@@ -23,7 +23,6 @@ namespace qf {
 namespace {
 
 constexpr int D = kHeadDim;
-constexpr int W = kMergeWaves;
 
 // fp32 -> bf16, round to nearest even; NaN stays a (quiet) NaN.
 __device__ __forceinline__ uint32_t bf16_rne(float f) {
@@ -35,7 +34,9 @@ __device__ __forceinline__ uint32_t bf16_rne(float f) {
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-template <bool BF16, bool CUR>
+// W wavefronts per workgroup: 4, or 16 for rows of more than 64 slots (each wavefront then still
+// makes one round of loads for up to 256 slots).
+template <bool BF16, bool CUR, int W>
 __global__ void __launch_bounds__(64 * W)
 merge_kernel(const float* __restrict__ in_o, const float* __restrict__ in_lse,
              void* __restrict__ out_o, float* __restrict__ out_lse, int32_t entries,
@@ -156,24 +157,30 @@ merge_kernel(const float* __restrict__ in_o, const float* __restrict__ in_lse,
   if (out_lse && lane == 0) out_lse[(size_t)r * hq + h] = lse_out;
 }
 
+template <int W>
+hipError_t launch_w(const MergeParams& p, bool to_bf16, unsigned grid, hipStream_t stream) {
+  if (p.q)
+    hipLaunchKernelGGL((merge_kernel<true, true, W>), dim3(grid), dim3(64 * W), 0, stream, p.in_o,
+                       p.in_lse, p.out_o, p.out_lse, p.entries, p.hq, p.q, p.k_cur, p.v_cur,
+                       p.hkv, p.scale);
+  else if (to_bf16)
+    hipLaunchKernelGGL((merge_kernel<true, false, W>), dim3(grid), dim3(64 * W), 0, stream,
+                       p.in_o, p.in_lse, p.out_o, p.out_lse, p.entries, p.hq, nullptr, nullptr,
+                       nullptr, 1, 0.0f);
+  else
+    hipLaunchKernelGGL((merge_kernel<false, false, W>), dim3(grid), dim3(64 * W), 0, stream,
+                       p.in_o, p.in_lse, p.out_o, p.out_lse, p.entries, p.hq, nullptr, nullptr,
+                       nullptr, 1, 0.0f);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_merge(const MergeParams& p, bool to_bf16, hipStream_t stream) {
   const unsigned grid = (unsigned)p.rows * (unsigned)p.hq;
   if (grid == 0) return hipSuccess;
-  if (p.q)
-    hipLaunchKernelGGL((merge_kernel<true, true>), dim3(grid), dim3(64 * W), 0, stream, p.in_o,
-                       p.in_lse, p.out_o, p.out_lse, p.entries, p.hq, p.q, p.k_cur, p.v_cur,
-                       p.hkv, p.scale);
-  else if (to_bf16)
-    hipLaunchKernelGGL((merge_kernel<true, false>), dim3(grid), dim3(64 * W), 0, stream, p.in_o,
-                       p.in_lse, p.out_o, p.out_lse, p.entries, p.hq, nullptr, nullptr, nullptr,
-                       1, 0.0f);
-  else
-    hipLaunchKernelGGL((merge_kernel<false, false>), dim3(grid), dim3(64 * W), 0, stream, p.in_o,
-                       p.in_lse, p.out_o, p.out_lse, p.entries, p.hq, nullptr, nullptr, nullptr,
-                       1, 0.0f);
-  return hipGetLastError();
+  return p.entries > 16 * kMergeWaves ? launch_w<16>(p, to_bf16, grid, stream)
+                                      : launch_w<kMergeWaves>(p, to_bf16, grid, stream);
 }
 
 }  // namespace qf

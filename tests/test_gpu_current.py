@@ -72,6 +72,16 @@ def test_fold_current_matches_oracle(gpu, Hq, Hkv):
         np.testing.assert_array_equal(out[2, h], v_new[2, h // G].float().cpu().numpy())
 
 
+def test_fold_over_many_shard_slots(gpu):
+    """The fold after a merge of 256 shard slots (the merge's 16-wavefront form)."""
+    case = _allocated_case(gpu, 2, 32, 8, [36000, 900], [256, 40], seed=205, max_shards=256)
+    k_new, v_new = _new_token(case, 206)
+    say("[current] fold over 256 slots")
+    out, lse = _fold_on_gpu(case, k_new, v_new)
+    ref_o, ref_l = _fold_reference(case, k_new, v_new)
+    _check_out("fold256", out, lse, ref_o, ref_l)
+
+
 def test_fold_either_sign_of_the_gap(gpu):
     """s_jj - lse_<j from -120 to +120 nats (short caches put the current token on top)."""
     gaps = np.array([-120.0, -30.0, -9.7, -1.0, 0.0, 1.0, 9.7, 30.0, 120.0])

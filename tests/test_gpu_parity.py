@@ -122,6 +122,17 @@ def test_planted_secondary_reading(gpu):
     assert np.all(np.abs(ref["lse"] - 85.0) < 1.5)
 
 
+def test_many_shard_slots_and_many_chunks(gpu):
+    """Rows of more than 64 slots (the merge's 16-wavefront form): 256 shard slots merged by the
+    combine, and one unit of a long cache cut into hundreds of chunks merged into its shard."""
+    case = make_case(2, 16, 8, [3000, 70000], [150, 200], seed=175, max_shards=256, device=gpu)
+    _run(case, "256 shard slots")
+    one = make_case(1, 1, 1, [100000], 1, seed=176, device=gpu)     # one unit: ~780 chunks
+    desc = qf.make_desc(one.q, one.k_cache, one.block_table, 1, one.scale)
+    assert qf.workspace_size(desc) > 64 * (128 + 1) * 4
+    _run(one, "one unit, many chunks")
+
+
 def test_out_of_range_device_values_poison_lse(gpu):
     """Out-of-range context length, shard count or block-table entry: the kernel clamps (no
     out-of-bounds access) and the affected request's lse becomes NaN; other requests are exact."""

@@ -254,8 +254,10 @@ class StageWorkload:
 STAGE_WORKLOADS = {
     w.name: w
     for w in [
-        StageWorkload("qwen3-0.6b_stage_b1_n4608", 11, "qwen3-0.6b", batch=1, ctx=4608, shards=8),
-        StageWorkload("qwen3-4b_stage_b1_n36480", 12, "qwen3-4b", batch=1, ctx=36480, shards=32),
+        # One request fills the GPU only when cut finely: as many shards as the sweep would
+        # otherwise make sub-shard chunks, so the current-token fold merges them directly.
+        StageWorkload("qwen3-0.6b_stage_b1_n4608", 11, "qwen3-0.6b", batch=1, ctx=4608, shards=32),
+        StageWorkload("qwen3-4b_stage_b1_n36480", 12, "qwen3-4b", batch=1, ctx=36480, shards=256),
     ]
 }
 
