@@ -184,9 +184,11 @@ def run_stage(args, dev):
         torch.cuda.synchronize()
         ms[name] = min(ms.get(name, float("inf")), t0.elapsed_time(t1) / K)
         log(f"[stage] {name}: {t0.elapsed_time(t1) / K:.4f} ms/step")
+    kernels = stage_kernel_times(stack, u, w, shape)
     if int(stack.status.item()) != 0:
         raise RuntimeError("a cache ran out of room during the stage bench")
-    print(json.dumps({
+    top = max(kernels, key=lambda k: kernels[k]["avg_us"] * kernels[k]["per_block"])
+    result = {
         "metric": "Q-First decode step, sweep beside the feed-forward (one shared launch)",
         "value": round(w.batch / (ms["fused"] * 1e-3), 1), "unit": "tokens/s",
         "n_gpus": 1, "steps": K, "warmup": W,
@@ -204,7 +206,106 @@ def run_stage(args, dev):
                    "n_kv_heads": shape.n_kv_heads, "ffn_bytes_per_layer": shape.ffn_bytes(),
                    "kv_bytes_per_layer": w.batch * w.ctx * kv_bytes_per_position(shape.n_kv_heads),
                    "graphs": True},
-    }), flush=True)
+        "kernels": kernels,
+        "roofline": {"bound": "hbm", "achieved": kernels[top]["GB/s"], "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(kernels[top]["GB/s"] / HBM_PEAK_GBS, 4),
+                     "kernel": top, "launch_avg_us": kernels[top]["avg_us"],
+                     "algorithmic_bytes": kernels[top]["bytes"], "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        log("[stage] cpu_baseline: timing the fp64 block oracle on a bounded sample")
+        result["cpu_baseline"] = stage_cpu_baseline(stack, u, w, shape)
+    print(json.dumps(result), flush=True)
+
+
+def stage_kernel_times(stack, u, w, shape, passes=2):
+    """Average GPU time of each launch of a block (shared-launch order), from HIP events around
+    every launch of an eager pass queued behind a GPU-side sleep (so the host's launch gaps are
+    not inside the events), with each launch's algorithmic bytes."""
+    import collections
+
+    import torch
+
+    spans = collections.defaultdict(list)
+
+    class Span:
+        def __init__(self, name):
+            self.name = name
+
+        def __enter__(self):
+            self.e0 = torch.cuda.Event(enable_timing=True)
+            self.e0.record()
+
+        def __exit__(self, *exc):
+            e1 = torch.cuda.Event(enable_timing=True)
+            e1.record()
+            spans[self.name].append((self.e0, e1))
+
+    n = int(stack.caches[0].ctx_lens.float().mean().item()) + passes // 2  # positions swept
+    stack.recorder = Span
+    try:
+        for _ in range(passes):
+            torch.cuda._sleep(200_000_000)          # ~0.1 s of GPU time to queue behind
+            stack.step(u, mode="fused")
+            torch.cuda.synchronize()
+    finally:
+        stack.recorder = None
+    B, H, I = w.batch, shape.hidden, shape.inter
+    Hq, Hkv, D, S = shape.n_q_heads, shape.n_kv_heads, 128, w.shards
+
+    def lin(N, K, xk=None, gain=True, res=False):
+        xk = K if xk is None else xk
+        return N * K * 2 + B * xk * 2 + (K * 2 if gain else 0) + B * N * 2 * (2 if res else 1)
+
+    partials = B * S * Hq * (D + 1) * 4
+    sweep = B * n * Hkv * D * 4 + B * (-(-n // 16)) * 4 + B * Hq * D * 2 + partials
+    nbytes = {
+        "W_q": lin(Hq * D, H),
+        "sweep + W_gate,W_up": sweep + lin(2 * I, H) - B * I * 2,    # writes the activation
+        "W_down": lin(H, I, gain=False, res=True),
+        "W_k,W_v": lin(2 * Hkv * D, H),
+        "merge + current-token fold": partials + B * Hq * D * 2 + 2 * B * Hkv * D * 2
+        + B * Hq * (D * 2 + 4),
+        "W_o": lin(H, Hq * D, gain=False, res=True),
+        "cache append": 4 * B * Hkv * D * 2 + 8 * B,
+    }
+    out = {}
+    for name, ev in spans.items():
+        avg_s = sum(a.elapsed_time(b) for a, b in ev) / len(ev) / 1e3
+        out[name] = {"avg_us": round(avg_s * 1e6, 2), "per_block": 1, "bytes": nbytes[name],
+                     "GB/s": round(nbytes[name] / avg_s / 1e9, 1)}
+    return out
+
+
+def stage_cpu_baseline(stack, u, w, shape, budget_s=10.0):
+    """The fp64 block oracle (oracle.qfirst_block) on the host, block after block from the same
+    seeded input, until about ``budget_s`` of CPU work; decode tokens per second of the stack."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import oracle
+
+    x = u.double().cpu().numpy()
+    blocks, spent = 0, 0.0
+    while spent < budget_s:
+        l = blocks % len(stack.layers)
+        c = stack.caches[l]
+        wts = {k: t.double().cpu().numpy() for k, t in stack.layers[l].items()
+               if k not in ("w_gu", "w_kv")}
+        kc, vc = c.k_cache.double().cpu().numpy(), c.v_cache.double().cpu().numpy()
+        bt, ctx = c.block_table.cpu().numpy(), np.full(w.batch, w.ctx)
+        t0 = time.perf_counter()
+        x = oracle.qfirst_block(x, wts, kc, vc, bt, ctx, shape.n_q_heads, shape.n_kv_heads,
+                                stack.scale)["y"]
+        spent += time.perf_counter() - t0
+        blocks += 1
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    steps = blocks / len(stack.layers)
+    return {"value": round(w.batch * steps / spent, 4), "unit": "tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{blocks} block(s) of the stack at context {w.ctx} (fp64 numpy, q/k/v, "
+                      f"feed-forward and attention over the cache plus the current token), "
+                      f"{spent:.1f} s; host has {len(os.sched_getaffinity(0))} usable cores"}
 
 
 def main():

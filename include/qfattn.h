@@ -206,15 +206,21 @@ int qf_schedule_simulate(int32_t n_requests, const double* arrival, const double
  * out [rows, n_split], the rest to out_b [rows, n_out - n_split] (one product can fill k and v);
  * residual: bf16 [rows, n_out] or NULL.  fp32 arithmetic, one round-to-nearest-even per output;
  * out must not alias x or residual.  Device pointers, caller-owned; asynchronous on `stream`.
+ * prologue | QF_LINEAR_GLU_OUT: the rows of W alternate the feed-forward's gate and up
+ * projections (row 2i = W_gate row i, row 2i + 1 = W_up row i), and the output is the activation
+ * itself, out[m, i] = silu(y[m, 2i]) * y[m, 2i + 1], bf16 [rows, n_out / 2] (computed once per
+ * element, from the fp32 sums); n_out must be even, n_split == n_out, residual NULL, and the
+ * prologue PLAIN or RMS_NORM.
  * Returns QF_OK; QF_EINVAL (rows < 0, n_out < 1, k < 8, unknown prologue, n_split outside
  * [1, n_out], eps < 0 or NaN with RMS_NORM, NULL x / w / out, NULL gain with RMS_NORM, NULL out_b
- * with n_split < n_out); QF_EUNSUPPORTED (rows > 8, k not a multiple of 8); QF_EALIGN (x, w, gain
- * not 16-byte aligned, out, out_b, residual not 2-byte aligned); QF_EHIP (launch failed).
- * rows == 0 is a no-op.
+ * with n_split < n_out, a GLU output without its conditions); QF_EUNSUPPORTED (rows > 8, k not a
+ * multiple of 8); QF_EALIGN (x, w, gain not 16-byte aligned, out, out_b, residual not 2-byte
+ * aligned); QF_EHIP (launch failed).  rows == 0 is a no-op.
  */
 #define QF_LINEAR_PLAIN 0
 #define QF_LINEAR_RMS_NORM 1
 #define QF_LINEAR_SWIGLU 2
+#define QF_LINEAR_GLU_OUT 16
 int qf_linear(int32_t rows, int32_t n_out, int32_t k, int32_t prologue, const void* x,
               const void* w, const void* gain, float eps, const void* residual, void* out,
               int32_t n_split, void* out_b, void* stream);

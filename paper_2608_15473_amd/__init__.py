@@ -12,6 +12,7 @@ from .binding import (  # noqa: F401
     QF_EHIP,
     QF_EINVAL,
     QF_EUNSUPPORTED,
+    QF_LINEAR_GLU_OUT,
     QF_LINEAR_PLAIN,
     QF_LINEAR_RMS_NORM,
     QF_LINEAR_SWIGLU,

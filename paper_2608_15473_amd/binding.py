@@ -20,7 +20,7 @@ EXPORTED = ("qf_attn_decode_split_workspace_size", "qf_attn_decode_split", "qf_a
             "qf_attn_combine_current", "qf_kv_append", "qf_linear", "qf_attn_decode_split_beside",
             "qf_schedule_simulate", "qf_last_error", "qf_version")
 QF_WIRING_QFIRST, QF_WIRING_COMPOSED = 0, 1
-QF_LINEAR_PLAIN, QF_LINEAR_RMS_NORM, QF_LINEAR_SWIGLU = 0, 1, 2
+QF_LINEAR_PLAIN, QF_LINEAR_RMS_NORM, QF_LINEAR_SWIGLU, QF_LINEAR_GLU_OUT = 0, 1, 2, 16
 
 
 class QFError(RuntimeError):
@@ -267,7 +267,7 @@ _PROLOGUES = {None: QF_LINEAR_PLAIN, "rms_norm": QF_LINEAR_RMS_NORM, "swiglu": Q
 
 
 def _linear_call(x, w, prologue=None, gain=None, eps=1e-6, residual=None, out=None, split=None,
-                 out_b=None):
+                 out_b=None, glu_out=False):
     """Checks and allocations of qf_linear: returns (LinearArgs, the output(s))."""
     if prologue not in _PROLOGUES:
         raise QFError(QF_EINVAL, f"unknown prologue {prologue!r}")
@@ -284,18 +284,22 @@ def _linear_call(x, w, prologue=None, gain=None, eps=1e-6, residual=None, out=No
         if tuple(residual.shape) != (M, N):
             raise QFError(QF_EINVAL, "residual must be [M, N]")
     n_split = N if split is None else int(split)
+    if glu_out and (N % 2 or n_split != N or residual is not None or prologue == "swiglu"):
+        raise QFError(QF_EINVAL, "glu_out needs an even N, no split, no residual, no swiglu input")
+    cols = N // 2 if glu_out else n_split
     if out is None:
-        out = torch.empty((M, n_split), dtype=torch.bfloat16, device=x.device)
+        out = torch.empty((M, cols), dtype=torch.bfloat16, device=x.device)
     if n_split < N and out_b is None:
         out_b = torch.empty((M, N - n_split), dtype=torch.bfloat16, device=x.device)
     _require(out, "out", torch.bfloat16)
-    if out.numel() != M * n_split:
-        raise QFError(QF_EINVAL, "out must hold [M, split] elements")
+    if out.numel() != M * cols:
+        raise QFError(QF_EINVAL, f"out must hold [M, {cols}] elements")
     if out_b is not None:
         _require(out_b, "out_b", torch.bfloat16)
         if out_b.numel() != M * (N - n_split):
             raise QFError(QF_EINVAL, "out_b must hold [M, N - split] elements")
-    la = LinearArgs(M, N, K, _PROLOGUES[prologue], x.data_ptr(), w.data_ptr(),
+    code = _PROLOGUES[prologue] | (QF_LINEAR_GLU_OUT if glu_out else 0)
+    la = LinearArgs(M, N, K, code, x.data_ptr(), w.data_ptr(),
                     None if gain is None else gain.data_ptr(), float(eps),
                     None if residual is None else residual.data_ptr(), out.data_ptr(), n_split,
                     None if out_b is None else out_b.data_ptr())
@@ -303,13 +307,14 @@ def _linear_call(x, w, prologue=None, gain=None, eps=1e-6, residual=None, out=No
 
 
 def linear(x, w, prologue=None, gain=None, eps=1e-6, residual=None, out=None, split=None,
-           out_b=None):
+           out_b=None, glu_out=False):
     """out = W . P(x) (+ residual) for up to 8 rows (qf_linear), all bf16.
 
     x [M, K] ([M, 2K] for "swiglu": gate, then up); w [N, K] (torch layout); prologue None,
     "rms_norm" (with ``gain`` [K]) or "swiglu".  With ``split`` the first ``split`` outputs go to
-    ``out`` [M, split] and the rest to ``out_b`` [M, N - split]."""
-    la, result = _linear_call(x, w, prologue, gain, eps, residual, out, split, out_b)
+    ``out`` [M, split] and the rest to ``out_b`` [M, N - split].  With ``glu_out`` the rows of w
+    alternate gate and up and the output is silu(gate) * up, [M, N / 2]."""
+    la, result = _linear_call(x, w, prologue, gain, eps, residual, out, split, out_b, glu_out)
     stream = torch.cuda.current_stream(x.device).cuda_stream
     _check(load_library().qf_linear(la.rows, la.n_out, la.k, la.prologue, la.x, la.w, la.gain,
                                     la.eps, la.residual, la.out, la.n_split, la.out_b,

@@ -4,21 +4,30 @@
 namespace qf {
 namespace {
 
-template <int PRO, int MB, int U>
+template <int PRO, int MB, int U, int R, bool GLU>
 __global__ void __launch_bounds__(lin::kThreads)
 linear_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
               const uint16_t* __restrict__ gain, const uint16_t* __restrict__ residual,
               uint16_t* __restrict__ out_a, uint16_t* __restrict__ out_b, int32_t M, int32_t N,
               int32_t K, int32_t n_split, float eps) {
-  lin::linear_rows<PRO, MB, U, 1>(x, w, gain, residual, out_a, out_b, M, N, K, n_split, eps,
-                                  blockIdx.x);
+  lin::linear_rows<PRO, MB, U, R, GLU>(x, w, gain, residual, out_a, out_b, M, N, K, n_split,
+                                       eps, blockIdx.x);
 }
 
+// One row per wavefront; two (a gate row and its up row) with the GLU output.
 template <int PRO, int MB, int U>
 void launch_u(const LinearParams& p, hipStream_t stream) {
-  const dim3 grid(lin::linear_blocks(p.N, 1));
-  hipLaunchKernelGGL((linear_kernel<PRO, MB, U>), grid, dim3(lin::kThreads), 0, stream, p.x,
-                     p.w, p.gain, p.residual, p.out_a, p.out_b, p.M, p.N, p.K, p.n_split, p.eps);
+  if constexpr (PRO != kProSwiglu) {   // the host rejects a GLU output after a SwiGLU input
+    if (p.glu) {
+      hipLaunchKernelGGL((linear_kernel<PRO, MB, U, 2, true>), dim3(lin::linear_blocks(p.N, 2)),
+                         dim3(lin::kThreads), 0, stream, p.x, p.w, p.gain, p.residual, p.out_a,
+                         p.out_b, p.M, p.N, p.K, p.n_split, p.eps);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((linear_kernel<PRO, MB, U, 1, false>), dim3(lin::linear_blocks(p.N, 1)),
+                     dim3(lin::kThreads), 0, stream, p.x, p.w, p.gain, p.residual, p.out_a,
+                     p.out_b, p.M, p.N, p.K, p.n_split, p.eps);
 }
 
 template <int PRO, int MB>

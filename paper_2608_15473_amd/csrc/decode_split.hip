@@ -377,7 +377,7 @@ sweep_beside_linear_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
     const uint16_t* __restrict__ gain, const uint16_t* __restrict__ residual,
     uint16_t* __restrict__ out_a, uint16_t* __restrict__ out_b, int32_t M, int32_t N, int32_t K,
-    int32_t n_split, float eps, int32_t prologue, int32_t linear_groups) {
+    int32_t n_split, float eps, int32_t prologue, int32_t glu, int32_t linear_groups) {
   static_assert(64 * kSplitWaves == lin::kThreads, "both roles use the same workgroup size");
   const unsigned j = blockIdx.x / 8u, lane8 = blockIdx.x % 8u;
   const unsigned long long S = (unsigned)units_per_xcd, T = S + (unsigned)linear_groups;
@@ -389,8 +389,17 @@ sweep_beside_linear_kernel(
                                               scale_log2, 8u * before + lane8);
     return;
   }
-  constexpr int U = 2, R = lin::beside_rows(MB);
+  constexpr int U = 2, R = lin::beside_rows(MB), RG = lin::beside_rows_glu(MB);
   const unsigned lb = 8u * (j - before) + lane8;
+  if (glu) {
+    if (prologue == kProRmsNorm)
+      lin::linear_rows<kProRmsNorm, MB, U, RG, true>(x, w, gain, residual, out_a, out_b, M, N, K,
+                                                     n_split, eps, lb);
+    else
+      lin::linear_rows<kProNone, MB, U, RG, true>(x, w, gain, residual, out_a, out_b, M, N, K,
+                                                  n_split, eps, lb);
+    return;
+  }
   if (prologue == kProRmsNorm)
     lin::linear_rows<kProRmsNorm, MB, U, R>(x, w, gain, residual, out_a, out_b, M, N, K, n_split,
                                             eps, lb);
@@ -404,14 +413,15 @@ sweep_beside_linear_kernel(
 
 template <int G, int MB>
 hipError_t launch_beside(const SplitParams& p, const LinearParams& l, hipStream_t stream) {
-  const int linear_groups = (lin::linear_blocks(l.N, lin::beside_rows(MB)) + 7) / 8;
+  const int rows = l.glu ? lin::beside_rows_glu(MB) : lin::beside_rows(MB);
+  const int linear_groups = (lin::linear_blocks(l.N, rows) + 7) / 8;
   const unsigned grid = 8u * ((unsigned)p.units_per_xcd + (unsigned)linear_groups);
   hipLaunchKernelGGL((sweep_beside_linear_kernel<G, MB>), dim3(grid), dim3(64 * kSplitWaves), 0,
                      stream, p.q, p.k, p.v, p.block_table, p.ctx_lens, p.n_shards, p.out_o,
                      p.out_lse, p.hq, p.hkv, p.max_pages, p.num_pages, p.max_shards, p.chunks,
                      p.n_units, p.units_per_xcd, p.batch, p.order, p.scale_log2, l.x, l.w, l.gain,
                      l.residual, l.out_a, l.out_b, l.M, l.N, l.K, l.n_split, l.eps, l.prologue,
-                     linear_groups);
+                     l.glu ? 1 : 0, linear_groups);
   return hipGetLastError();
 }
 

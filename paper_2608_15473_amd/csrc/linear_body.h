@@ -46,7 +46,10 @@ __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
 // U: 512-element chunks of K each wavefront loads per group before using any; R: output rows per
 // wavefront, all fed by the same input chunks (loaded and transformed once).  Neither changes the
 // arithmetic: every lane accumulates each row's chunks in the same order for any U and R.
-template <int PRO, int MB, int U, int R>
+// GLU: the rows of W alternate gate and up (row 2i = gate i, 2i + 1 = up i; R even), and the
+// output is the feed-forward's activation out[m, i] = silu(y[m, 2i]) * y[m, 2i + 1] (N / 2
+// columns), computed once per element instead of in every row of the product that consumes it.
+template <int PRO, int MB, int U, int R, bool GLU = false>
 __device__ __forceinline__ void linear_rows(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
     const uint16_t* __restrict__ gain, const uint16_t* __restrict__ residual,
@@ -155,6 +158,24 @@ __device__ __forceinline__ void linear_rows(
       if (PRO == kProRmsNorm) acc[r][m] *= scale;
     }
   }
+  if (GLU) {
+    static_assert(!GLU || R % 2 == 0, "gate and up rows come in pairs");
+    if (lane < M) {
+#pragma unroll
+      for (int r = 0; r < R; r += 2) {
+        if (n0 + r + 1 >= N) break;
+        float g = 0.0f, v = 0.0f;
+#pragma unroll
+        for (int m = 0; m < MB; ++m)
+          if (m == lane) {
+            g = acc[r][m];
+            v = acc[r + 1][m];
+          }
+        out_a[(size_t)lane * (N / 2) + (n0 + r) / 2] = (uint16_t)bf16_rne(silu(g) * v);
+      }
+    }
+    return;
+  }
   if (lane < M) {
 #pragma unroll
     for (int r = 0; r < R; ++r) {
@@ -180,6 +201,7 @@ inline int linear_blocks(int N, int R) { return (N + kRowsPerBlock * R - 1) / (k
 // R for the shared launch with the sweep, where the product's workgroups run at the sweep's
 // occupancy: more rows per wavefront keep enough weight bytes in flight.
 constexpr int beside_rows(int MB) { return MB <= 2 ? 4 : MB <= 4 ? 2 : 1; }
+constexpr int beside_rows_glu(int MB) { return MB <= 2 ? 4 : 2; }
 
 // U for a row length K: enough chunks to cover K in one group where registers allow (at most 8
 // loads of weights plus 8 of inputs per lane).

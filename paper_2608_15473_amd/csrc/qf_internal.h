@@ -79,6 +79,7 @@ struct LinearParams {
   uint16_t* out_b;           // bf16 [M, N - n_split]
   int M, N, K, n_split, prologue;
   float eps;
+  bool glu;                  // rows of W alternate gate / up; out = silu(gate) * up, N / 2 columns
 };
 hipError_t launch_linear(const LinearParams& p, hipStream_t stream);
 // The sweep and a fused product in one launch (decode_split.hip).

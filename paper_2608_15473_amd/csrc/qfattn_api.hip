@@ -166,7 +166,9 @@ int finish_split(const Split& sp, hipStream_t s) {
 
 // Everything qf_linear checks and derives before launching.
 int prepare_linear(const qf_linear_args* a, qf::LinearParams* out_p, bool* noop) {
-  const int32_t rows = a->rows, n_out = a->n_out, k = a->k, prologue = a->prologue;
+  const int32_t rows = a->rows, n_out = a->n_out, k = a->k;
+  const bool glu = (a->prologue & QF_LINEAR_GLU_OUT) != 0;
+  const int32_t prologue = a->prologue & ~QF_LINEAR_GLU_OUT;
   const int32_t n_split = a->n_split;
   const void *x = a->x, *w = a->w, *gain = a->gain, *residual = a->residual;
   void *out = a->out, *out_b = a->out_b;
@@ -181,6 +183,9 @@ int prepare_linear(const qf_linear_args* a, qf::LinearParams* out_p, bool* noop)
     return fail(QF_EINVAL, "unknown prologue %d", prologue);
   if (n_split < 1 || n_split > n_out)
     return fail(QF_EINVAL, "n_split must be in [1, n_out] (got %d)", n_split);
+  if (glu && (prologue == QF_LINEAR_SWIGLU || n_out % 2 || n_split != n_out || a->residual))
+    return fail(QF_EINVAL, "QF_LINEAR_GLU_OUT needs an even n_out, n_split == n_out, no residual "
+                           "and no SwiGLU input");
   if (prologue == QF_LINEAR_RMS_NORM && !(eps >= 0.0f)) return fail(QF_EINVAL, "eps must be >= 0");
   if (rows == 0) {
     *noop = true;
@@ -207,6 +212,7 @@ int prepare_linear(const qf_linear_args* a, qf::LinearParams* out_p, bool* noop)
              : prologue == QF_LINEAR_SWIGLU   ? qf::kProSwiglu
                                               : qf::kProNone;
   p.eps = eps;
+  p.glu = glu;
   *out_p = p;
   return QF_OK;
 }

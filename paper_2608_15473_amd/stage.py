@@ -9,7 +9,7 @@ the two may run at once.  On one GPU this module offers three orders of the same
   mode="serial":   everything on one stream, in the order drawn below;
   mode="streams":  the sweep on a second HIP stream, forked after q and joined before the fold:
 
-    main stream:       W_q N1(u) -> q --+--> W_gate|W_up N2(u) -> u + W_down SwiGLU(.) = z
+    main stream:       W_q N1(u) -> q --+--> SwiGLU(W_gate|W_up N2(u)) -> u + W_down(.) = z
                                         |     -> W_k|W_v N1(z) -> k, v --[join]--> merge + fold
                                         |                              -> z + W_o attn = y; append
     attention stream:                   +--> sweep of the layer's cache (split into shards) --^
@@ -26,6 +26,7 @@ outputs and caches.  Every buffer is allocated once, so a step can be captured i
 
 from __future__ import annotations
 
+import contextlib
 import dataclasses
 
 import torch
@@ -72,7 +73,9 @@ class QFirstStack:
             if missing:
                 raise ValueError(f"missing weights {missing}")
             lw = dict(w)                                    # one product each for gate|up, k|v
-            lw["w_gu"] = torch.cat([w["w_gate"], w["w_up"]], 0).contiguous()
+            # gate and up rows interleaved, so the product's epilogue writes the activation
+            lw["w_gu"] = torch.stack([w["w_gate"], w["w_up"]], 1).reshape(
+                -1, w["w_gate"].shape[1]).contiguous()
             lw["w_kv"] = torch.cat([w["w_k"], w["w_v"]], 0).contiguous()
             self.layers.append(lw)
         self.caches = list(caches)
@@ -87,7 +90,7 @@ class QFirstStack:
         self.y = [buf(B, H), buf(B, H)]                       # ping-pong between layers
         self.q = buf(B, self.hq, D)
         self.k, self.v = buf(B, self.hkv, D), buf(B, self.hkv, D)
-        self.gu = buf(B, 2 * I)
+        self.act = buf(B, I)                                  # silu(gate) * up
         self.attn = buf(B, self.hq, D)
         self.lse = buf(B, self.hq, dtype=torch.float32)
         self.part_out = buf(B, self.max_shards, self.hq, D, dtype=torch.float32)
@@ -97,6 +100,12 @@ class QFirstStack:
                                                 self.max_shards, self.scale))
                  for c in self.caches)
         self.workspace = buf(max(ws, 1), dtype=torch.uint8) if ws else None
+        # Optional: a callable name -> context manager wrapped around every launch of a block
+        # (e.g. HIP events on the current stream, to time each kernel).
+        self.recorder = None
+
+    def _span(self, name: str):
+        return contextlib.nullcontext() if self.recorder is None else self.recorder(name)
 
     # ----------------------------------------------------------------------------------------
     def _sweep(self, c: LayerCache) -> None:
@@ -105,14 +114,15 @@ class QFirstStack:
                              part_out=self.part_out, part_lse=self.part_lse,
                              workspace=self.workspace)
 
-    def _linear(self, x, w, out, prologue=None, gain=None, residual=None, out_b=None):
+    def _linear(self, x, w, out, prologue=None, gain=None, residual=None, out_b=None,
+                glu_out=False):
         """qf_linear over the batch in blocks of at most 8 rows."""
         B, split = self.B, out.shape[-1] if out_b is not None else None
         for r in range(0, B, 8):
             e = min(B, r + 8)
             qf.linear(x[r:e], w, prologue, gain, self.eps,
                       residual=None if residual is None else residual[r:e], out=out[r:e],
-                      split=split, out_b=None if out_b is None else out_b[r:e])
+                      split=split, out_b=None if out_b is None else out_b[r:e], glu_out=glu_out)
 
     def block(self, l: int, u: torch.Tensor, out: torch.Tensor, mode: str = "fused"):
         """One Q-First block: reads u [B, H], writes out [B, H], appends the layer's (k, v)."""
@@ -121,35 +131,45 @@ class QFirstStack:
         w, c = self.layers[l], self.caches[l]
         B = self.B
         main = torch.cuda.current_stream(self.device)
-        self._linear(u, w["w_q"], self.q.view(B, -1), "rms_norm", w["g1"])   # q reads u
+        with self._span("W_q"):                                             # q reads u
+            self._linear(u, w["w_q"], self.q.view(B, -1), "rms_norm", w["g1"])
         if mode == "fused":                                                  # sweep | W_gate|W_up
             head = min(B, 8)
-            qf.attn_decode_split_beside(
-                self.q, c.k_cache, c.v_cache, c.block_table, c.ctx_lens, c.n_shards,
-                dict(x=u[:head], w=w["w_gu"], prologue="rms_norm", gain=w["g2"], eps=self.eps,
-                     out=self.gu[:head]),
-                max_shards=self.max_shards, scale=self.scale, part_out=self.part_out,
-                part_lse=self.part_lse, workspace=self.workspace)
-            if B > head:
-                self._linear(u[head:], w["w_gu"], self.gu[head:], "rms_norm", w["g2"])
+            with self._span("sweep + W_gate,W_up"):
+                qf.attn_decode_split_beside(
+                    self.q, c.k_cache, c.v_cache, c.block_table, c.ctx_lens, c.n_shards,
+                    dict(x=u[:head], w=w["w_gu"], prologue="rms_norm", gain=w["g2"], eps=self.eps,
+                         out=self.act[:head], glu_out=True),
+                    max_shards=self.max_shards, scale=self.scale, part_out=self.part_out,
+                    part_lse=self.part_lse, workspace=self.workspace)
+                if B > head:
+                    self._linear(u[head:], w["w_gu"], self.act[head:], "rms_norm", w["g2"],
+                                 glu_out=True)
         else:
             if mode == "streams":
                 self.attn_stream.wait_stream(main)
-                with torch.cuda.stream(self.attn_stream):
+                with torch.cuda.stream(self.attn_stream), self._span("sweep"):
                     self._sweep(c)
             else:
-                self._sweep(c)
-            self._linear(u, w["w_gu"], self.gu, "rms_norm", w["g2"])         # the feed-forward
-        self._linear(self.gu, w["w_down"], self.z, "swiglu", residual=u)     # z = u + M(N2 u)
-        self._linear(self.z, w["w_kv"], self.k.view(B, -1), "rms_norm", w["g1"],
-                     out_b=self.v.view(B, -1))                              # k, v read z
+                with self._span("sweep"):
+                    self._sweep(c)
+            with self._span("W_gate,W_up"):                                  # the feed-forward
+                self._linear(u, w["w_gu"], self.act, "rms_norm", w["g2"], glu_out=True)
+        with self._span("W_down"):                                           # z = u + M(N2 u)
+            self._linear(self.act, w["w_down"], self.z, residual=u)
+        with self._span("W_k,W_v"):                                          # k, v read z
+            self._linear(self.z, w["w_kv"], self.k.view(B, -1), "rms_norm", w["g1"],
+                         out_b=self.v.view(B, -1))
         if mode == "streams":
             main.wait_stream(self.attn_stream)
-        qf.attn_combine_current(self.part_out, self.part_lse, self.q, self.k, self.v,
-                                scale=self.scale, out=self.attn, lse=self.lse)
-        self._linear(self.attn.view(B, -1), w["w_o"], out, residual=self.z)  # y = z + W_o attn
-        qf.kv_append(c.k_cache, c.v_cache, c.block_table, c.ctx_lens, self.k, self.v,
-                     advance=True, status=self.status)
+        with self._span("merge + current-token fold"):
+            qf.attn_combine_current(self.part_out, self.part_lse, self.q, self.k, self.v,
+                                    scale=self.scale, out=self.attn, lse=self.lse)
+        with self._span("W_o"):                                              # y = z + W_o attn
+            self._linear(self.attn.view(B, -1), w["w_o"], out, residual=self.z)
+        with self._span("cache append"):
+            qf.kv_append(c.k_cache, c.v_cache, c.block_table, c.ctx_lens, self.k, self.v,
+                         advance=True, status=self.status)
         return out
 
     def step(self, u: torch.Tensor, mode: str = "fused") -> torch.Tensor:

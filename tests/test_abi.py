@@ -167,6 +167,12 @@ def test_linear_rejects_bad_arguments():
     assert f(2, 64, 64, P, a, a, None, 0.0, ctypes.c_void_p(4097), a, 64, None,
              None) == qf.QF_EALIGN
     assert f(0, 64, 64, P, None, None, None, 0.0, None, None, 64, None, None) == qf.QF_OK
+    G = qf.QF_LINEAR_GLU_OUT
+    assert f(2, 63, 64, R | G, a, a, a, 1e-6, None, a, 63, None, None) == qf.QF_EINVAL   # odd
+    assert f(2, 64, 64, R | G, a, a, a, 1e-6, a, a, 64, None, None) == qf.QF_EINVAL     # residual
+    assert f(2, 64, 64, R | G, a, a, a, 1e-6, None, a, 32, a, None) == qf.QF_EINVAL     # split
+    assert f(2, 64, 64, S | G, a, a, None, 0.0, None, a, 64, None, None) == qf.QF_EINVAL  # swiglu in
+    assert f(2, 64, 64, 4 | G, a, a, None, 0.0, None, a, 64, None, None) == qf.QF_EINVAL  # unknown
 
 
 def test_beside_checks_both_calls_before_launching():

@@ -112,17 +112,48 @@ def test_linear_matches_oracle(gpu, M, N, K, pro, res, split):
     assert ok.all(), (np.argwhere(~ok)[:4], out[~ok][:4], ref[~ok][:4])
 
 
-BESIDE_CASES = [  # (B, Hq, Hkv, ctx, shards, M, N, K, prologue)
-    (1, 16, 8, [4608], 8, 1, 6144, 1024, "rms_norm"),       # chunked sweep (few units)
-    (4, 32, 8, [900, 17, 3000, 0], 3, 4, 2056, 512, "rms_norm"),
-    (3, 8, 8, [300, 1, 77], 2, 8, 1001, 264, None),
-    (2, 64, 8, [5000, 40], [6, 1], 3, 1024, 3072, "swiglu"),
-    (2, 16, 4, [128, 2048], 64, 2, 520, 1024, "rms_norm"),   # unchunked: many units
+@pytest.mark.parametrize("M,I,K", [(1, 3072, 1024), (3, 9728, 2560), (8, 24, 520)])
+def test_linear_glu_output_matches_oracle(gpu, M, I, K):
+    """Rows of W alternating gate and up, output silu(gate) * up from the fp32 sums: within the
+    bf16 values around the exact activation widened by the accumulation bounds of both sums
+    carried through silu (|silu'| <= 1.1) and the product."""
+    gen = torch.Generator().manual_seed(M * 31 + I + K)
+    x = (torch.randn(M, K, generator=gen) * 2).to(torch.bfloat16)
+    wg = (torch.randn(I, K, generator=gen) / K ** 0.5).to(torch.bfloat16)
+    wu = (torch.randn(I, K, generator=gen) / K ** 0.5).to(torch.bfloat16)
+    g = (torch.rand(K, generator=gen) + 0.5).to(torch.bfloat16)
+    w = torch.stack([wg, wu], 1).reshape(2 * I, K).contiguous()
+    say(f"[stage] linear GLU M={M} I={I} K={K}")
+    got = qf.linear(x.to(gpu), w.to(gpu), "rms_norm", g.to(gpu), 1e-6, glu_out=True)
+    torch.cuda.synchronize()
+    assert tuple(got.shape) == (M, I)
+    px = oracle.rms_norm(x.double().numpy(), g.double().numpy(), 1e-6)
+    G, U = px @ wg.double().numpy().T, px @ wu.double().numpy().T
+    ref = oracle.swiglu(G, U)
+    eps = (K / 64 + 32) * 2.0 ** -24
+    dG = eps * (np.abs(px) @ np.abs(wg.double().numpy()).T)
+    dU = eps * (np.abs(px) @ np.abs(wu.double().numpy()).T)
+    delta = 1.1 * np.abs(U) * dG + np.abs(oracle.silu(G)) * dU + 1e-6 * np.abs(ref)
+    lo, _ = bf16_neighbours(ref - delta)
+    _, hi = bf16_neighbours(ref + delta)
+    out = got.double().cpu().numpy()
+    ok = (out >= lo) & (out <= hi)
+    assert ok.all(), (np.argwhere(~ok)[:4], out[~ok][:4], ref[~ok][:4])
+
+
+BESIDE_CASES = [  # (B, Hq, Hkv, ctx, shards, M, N, K, prologue, GLU output)
+    (1, 16, 8, [4608], 8, 1, 6144, 1024, "rms_norm", False),       # chunked sweep (few units)
+    (1, 16, 8, [4608], 32, 1, 6144, 1024, "rms_norm", True),       # the stage's shared launch
+    (4, 32, 8, [900, 17, 3000, 0], 3, 4, 2056, 512, "rms_norm", False),
+    (3, 8, 8, [300, 1, 77], 2, 8, 1001, 264, None, False),
+    (3, 8, 8, [300, 1, 77], 2, 8, 1002, 264, None, True),
+    (2, 64, 8, [5000, 40], [6, 1], 3, 1024, 3072, "swiglu", False),
+    (2, 16, 4, [128, 2048], 64, 2, 520, 1024, "rms_norm", False),  # unchunked: many units
 ]
 
 
-@pytest.mark.parametrize("B,Hq,Hkv,ctx,shards,M,N,K,pro", BESIDE_CASES)
-def test_beside_equals_the_two_calls_bitwise(gpu, B, Hq, Hkv, ctx, shards, M, N, K, pro):
+@pytest.mark.parametrize("B,Hq,Hkv,ctx,shards,M,N,K,pro,glu", BESIDE_CASES)
+def test_beside_equals_the_two_calls_bitwise(gpu, B, Hq, Hkv, ctx, shards, M, N, K, pro, glu):
     case = make_case(B, Hq, Hkv, ctx, shards, seed=800 + Hq + M, device=gpu)
     gen = torch.Generator(device=gpu).manual_seed(801 + N)
     x = torch.randn(M, 2 * K if pro == "swiglu" else K, generator=gen, device=gpu).to(torch.bfloat16)
@@ -134,9 +165,9 @@ def test_beside_equals_the_two_calls_bitwise(gpu, B, Hq, Hkv, ctx, shards, M, N,
     for together in (False, True):
         po = torch.full((B, S, Hq, 128), float("nan"), device=gpu)
         pl = torch.full((B, S, Hq), float("nan"), device=gpu)
-        y = torch.full((M, N), float("nan"), device=gpu).to(torch.bfloat16)
-        lin = dict(x=x, w=w, prologue=pro, gain=g if pro == "rms_norm" else None, residual=res,
-                   out=y)
+        y = torch.full((M, N // 2 if glu else N), float("nan"), device=gpu).to(torch.bfloat16)
+        lin = dict(x=x, w=w, prologue=pro, gain=g if pro == "rms_norm" else None,
+                   residual=None if glu else res, out=y, glu_out=glu)
         say(f"[stage] beside B={B} G={Hq // Hkv} M={M} N={N} K={K} together={together}")
         sweep = (case.q, case.k_cache, case.v_cache, case.block_table, case.ctx_lens,
                  case.n_shards)
