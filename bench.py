@@ -1,8 +1,9 @@
 """Decode-attention bench: split-KV GQA sweep + LSE combine over every layer of a workload.
 
 One step = for every layer: qf_attn_decode_split (sweep of all cached K/V, per-shard (O, ln Z))
-then qf_attn_combine (merge to bf16 out + fp32 lse).  All layers' inputs are resident in HBM
-before the timed region.  Prints ONE JSON line.
+then qf_attn_combine (merge to bf16 out + fp32 lse); with --one-launch both in one launch
+(qf_attn_decode).  All layers' inputs are resident in HBM before the timed region.  Prints ONE
+JSON line.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 
@@ -58,18 +59,20 @@ def algorithmic_bytes(case):
     return dict(kv=kv, sweep=sweep, combine=combine, attended=int(n.sum()))
 
 
-def committed_traffic(workload):
-    """HBM bytes per sweep launch from the committed rocprofv3 counter summary of this workload,
-    or None when there is none or the sweep kernel's sources changed since it was taken."""
+def committed_traffic(workload, two_launch=False):
+    """HBM bytes per launch of the timed kernel (the one-launch sweep + merge, or the sweep of
+    the two-launch step) from the committed rocprofv3 counter summary of this workload, or None
+    when there is none or the kernel's sources changed since it was taken."""
     import hashlib
 
-    path = os.path.join(ROOT, "profiles", f"decode_split_{workload}_hbm_traffic.json")
+    kind = "decode_split" if two_launch else "decode_fused"
+    path = os.path.join(ROOT, "profiles", f"{kind}_{workload}_hbm_traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
     h = hashlib.sha256()
-    for name in ("decode_split.hip", "linear_body.h", "qf_internal.h"):
+    for name in ("decode_split.hip", "linear_body.h", "merge_body.h", "qf_internal.h"):
         with open(os.path.join(ROOT, "paper_2608_15473_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     if h.hexdigest() != rec.get("kernel_source_sha256"):
@@ -320,6 +323,9 @@ def main():
     ap.add_argument("--layers", type=int, default=None,
                     help="resident layers (default: the workload's own count)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--one-launch", action="store_true",
+                    help="sweep and merge in one launch (qf_attn_decode): faster only where "
+                         "launches dominate (small steps)")
     ap.add_argument("--stage", default=None,
                     help="time the [MLP || Attn] decode stage of this block workload instead")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -372,8 +378,9 @@ def main():
     out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=dev)
     lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
     desc = qf.make_desc(cases[0].q, cases[0].k_cache, cases[0].block_table, S, cases[0].scale)
-    need = qf.workspace_size(desc)
+    need = qf.decode_workspace_size(desc) if args.one_launch else qf.workspace_size(desc)
     ws = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    counters = torch.zeros(B * Hkv, dtype=torch.int32, device=dev)  # zero-filled once
 
     turn = [0]
 
@@ -384,12 +391,18 @@ def main():
             c = cases[(base + l) % copies]
             if events is not None:
                 events[l][0].record()
-            qf.attn_decode_split(c.q, c.k_cache, c.v_cache, c.block_table, c.ctx_lens,
-                                 c.n_shards, max_shards=S, scale=c.scale, part_out=po,
-                                 part_lse=pl, workspace=ws)
+            if not args.one_launch:
+                qf.attn_decode_split(c.q, c.k_cache, c.v_cache, c.block_table, c.ctx_lens,
+                                     c.n_shards, max_shards=S, scale=c.scale, part_out=po,
+                                     part_lse=pl, workspace=ws)
+            else:
+                qf.attn_decode(c.q, c.k_cache, c.v_cache, c.block_table, c.ctx_lens,
+                               c.n_shards, max_shards=S, scale=c.scale, out=out, lse=lse,
+                               workspace=ws, counters=counters)
             if events is not None:
                 events[l][1].record()
-            qf.attn_combine(po, pl, out=out, lse=lse)
+            if not args.one_launch:
+                qf.attn_combine(po, pl, out=out, lse=lse)
 
     warm, t_w = 0, time.perf_counter()
     while (warm < args.warmup) if args.warmup is not None else \
@@ -421,7 +434,7 @@ def main():
     kv_step = sum(a["kv"] for a in ab)
     value = kv_step / (ms_per_step / 1e3) / 1e9
     attended = sum(a["attended"] for a in ab) / L
-    sweep_bytes = sum(a["sweep"] for a in ab) / L
+    sweep_bytes = sum(a["sweep"] + (a["combine"] if args.one_launch else 0) for a in ab) / L
     achieved = sweep_bytes / sweep_avg_s / 1e9
     result = {
         "metric": "decode-attention KV GB/s (and % of HBM peak); attended tokens/s per layer",
@@ -436,7 +449,8 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": w.name, "batch": B, "n_q_heads": Hq, "n_kv_heads": Hkv,
+        "config": {"workload": w.name, "launches_per_layer": 1 if args.one_launch else 2,
+                   "batch": B, "n_q_heads": Hq, "n_kv_heads": Hkv,
                    "head_dim": D, "page": 16, "layers": L, "max_shards": S,
                    "context": w.ctx if w.ctx else "ragged", "kv_dtype": "bf16",
                    "kv_bytes_per_step": kv_step, "workspace_bytes": need,
@@ -445,9 +459,11 @@ def main():
         "attended_tokens_per_s_per_layer": round(attended / (ms_per_step / 1e3 / L), 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "kernel": "decode_split_kernel", "launch_avg_us": round(sweep_avg_s * 1e6, 2),
+                     "kernel": "decode_fused_kernel" if args.one_launch else "decode_split_kernel",
+                     "launch_avg_us": round(sweep_avg_s * 1e6, 2),
                      "algorithmic_bytes": int(sweep_bytes),
-                     "traffic": committed_traffic(w.name) if L == w.layers else None},
+                     "traffic": committed_traffic(w.name, not args.one_launch)
+                     if L == w.layers else None},
     }
     if not args.no_cpu_baseline:
         log("[bench] cpu_baseline: timing the fp64 oracle on a bounded sample")

@@ -12,7 +12,8 @@
  * and the pairs of all shards merge into the result of one sweep over the whole cache (§5: any
  * partition, any order; an empty shard is ln Z = -inf with a vector that is never read).
  *
- * Entry points: the sweep and its merge (qf_attn_decode_split, qf_attn_combine); the decode step
+ * Entry points: the sweep and its merge (qf_attn_decode_split, qf_attn_combine, or both in one
+ * launch: qf_attn_decode); the decode step
  * around them (qf_attn_combine_current folds in the current token, qf_kv_append writes it to the
  * cache); the dense products of a decoder block (qf_linear) and the sweep sharing one launch with
  * one of them (qf_attn_decode_split_beside); and a host-side simulation of the layer-wise decode
@@ -103,6 +104,37 @@ int qf_attn_decode_split(const qf_decode_desc* desc, const void* q, const void* 
                          const void* v_cache, const int32_t* block_table,
                          const int32_t* ctx_lens, const int32_t* n_shards, float* part_out,
                          float* part_lse, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The sweep and the merge in ONE launch: the result of qf_attn_decode_split followed by
+ * qf_attn_combine on the same inputs, without materialising the per-shard outputs in caller
+ * buffers.  Bitwise the same when the shape needs no sub-shard chunks
+ * (qf_attn_decode_split_workspace_size() == 0) and max_shards <= 64; otherwise the slots are
+ * grouped differently (the chunks of every shard merge in the same pass as the shards; more than
+ * 64 slots are summed by 4 wavefronts instead of 16), which can move the last bits.  The last workgroup to finish a (request, KV head) merges that group's slots
+ * (partial states stay in the workspace), so the merge's launch and its wait for the sweep's
+ * tail disappear.
+ *
+ *   q ... n_shards   as for qf_attn_decode_split.
+ *   out              bf16 [B, Hq, D], 4-byte aligned; lse fp32 [B, Hq] natural log, or NULL.
+ *                    Values as for qf_attn_combine.
+ *   workspace        device buffer of at least qf_attn_decode_workspace_size() bytes (the
+ *                    partial states), 16-byte aligned; no initialisation needed.
+ *   counters         int32 device array of n_counters >= B * Hkv entries, 4-byte aligned, one
+ *                    per (request, KV head).  It must be ZERO-FILLED before its first use; every
+ *                    call leaves the entries it used at zero again, so an array zero-filled once
+ *                    serves any number of calls with any descriptor (as long as it is large
+ *                    enough).  Calls that share a workspace or counters must not run
+ *                    concurrently.
+ * Returns the codes of qf_attn_decode_split; QF_EINVAL also for a NULL out, workspace or
+ * counters, a workspace that is too small or too few counters.
+ */
+int qf_attn_decode_workspace_size(const qf_decode_desc* desc, size_t* bytes);
+int qf_attn_decode(const qf_decode_desc* desc, const void* q, const void* k_cache,
+                   const void* v_cache, const int32_t* block_table, const int32_t* ctx_lens,
+                   const int32_t* n_shards, void* out, float* lse, void* workspace,
+                   size_t workspace_bytes, int32_t* counters, int64_t n_counters,
+                   void* stream);
 
 /*
  * The merge of §5 over every shard slot: for each request b and query head h,

@@ -25,6 +25,7 @@ from .binding import (  # noqa: F401
     attn_decode,
     attn_decode_split,
     attn_decode_split_beside,
+    decode_workspace_size,
     kv_append,
     load_library,
     schedule_simulate,

@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(_HERE, "lib", "libqfattn.so")
 
 QF_OK, QF_EINVAL, QF_EUNSUPPORTED, QF_EALIGN, QF_EHIP = 0, -1, -2, -3, -4
 EXPORTED = ("qf_attn_decode_split_workspace_size", "qf_attn_decode_split", "qf_attn_combine",
+            "qf_attn_decode_workspace_size", "qf_attn_decode",
             "qf_attn_combine_current", "qf_kv_append", "qf_linear", "qf_attn_decode_split_beside",
             "qf_schedule_simulate", "qf_last_error", "qf_version")
 QF_WIRING_QFIRST, QF_WIRING_COMPOSED = 0, 1
@@ -62,6 +63,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.qf_attn_decode_split.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp, vp, vp,
                                          vp, vp, sz, vp]
     lib.qf_attn_combine.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp]
+    lib.qf_attn_decode_workspace_size.argtypes = [ctypes.POINTER(DecodeDesc), ctypes.POINTER(sz)]
+    lib.qf_attn_decode.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                   sz, vp, ctypes.c_int64, vp]
     lib.qf_attn_combine_current.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, vp,
                                             ctypes.c_float, vp, vp, vp]
     lib.qf_kv_append.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp, vp, i32, vp, vp]
@@ -76,6 +80,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.qf_last_error.argtypes = []
     lib.qf_version.argtypes = []
     for name in ("qf_attn_decode_split_workspace_size", "qf_attn_decode_split",
+                 "qf_attn_decode_workspace_size", "qf_attn_decode",
                  "qf_attn_combine", "qf_attn_combine_current", "qf_kv_append",
                  "qf_linear", "qf_attn_decode_split_beside", "qf_schedule_simulate", "qf_version"):
         getattr(lib, name).restype = ctypes.c_int
@@ -322,13 +327,60 @@ def linear(x, w, prologue=None, gain=None, eps=1e-6, residual=None, out=None, sp
     return result
 
 
+def decode_workspace_size(desc: DecodeDesc) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load_library().qf_attn_decode_workspace_size(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value
+
+
 def attn_decode(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards=None,
-                scale=None):
-    """Sweep then merge: (out bf16 [B, Hq, D], lse fp32 [B, Hq], part_out, part_lse)."""
-    po, pl = attn_decode_split(q, k_cache, v_cache, block_table, ctx_lens, n_shards,
-                               max_shards=max_shards, scale=scale)
-    out, lse = attn_combine(po, pl)
-    return out, lse, po, pl
+                scale=None, out=None, lse=None, workspace=None, counters=None, max_pages=None,
+                want_lse=True):
+    """Sweep and merge in one launch (qf_attn_decode): returns (out bf16 [B, Hq, D],
+    lse fp32 [B, Hq]), those of ``attn_combine(*attn_decode_split(...))`` (bitwise when the
+    shape needs no sub-shard chunks and has at most 64 shard slots; otherwise the slots are
+    grouped differently, which can move the last bits).
+
+    ``workspace``: uint8 tensor of at least ``decode_workspace_size`` bytes (allocated when
+    None); ``counters``: int32 tensor of at least B * Hkv entries, zero-filled before its first
+    use (every call leaves it at zero; allocated zeroed when None)."""
+    _require(q, "q", torch.bfloat16, 3)
+    _require(k_cache, "k_cache", torch.bfloat16, 4)
+    _require(v_cache, "v_cache", torch.bfloat16, 4)
+    if v_cache.shape != k_cache.shape:
+        raise QFError(QF_EINVAL, "k_cache and v_cache shapes differ")
+    if block_table is not None:
+        _require(block_table, "block_table", torch.int32, 2)
+    _require(ctx_lens, "ctx_lens", torch.int32, 1)
+    B, Hq, D = q.shape
+    if isinstance(n_shards, int):
+        if max_shards is None:
+            max_shards = n_shards
+        n_shards = torch.full((B,), n_shards, dtype=torch.int32, device=q.device)
+    _require(n_shards, "n_shards", torch.int32, 1)
+    if max_shards is None:
+        raise QFError(QF_EINVAL, "max_shards is required when n_shards is a tensor")
+    if scale is None:
+        scale = D ** -0.5
+    desc = make_desc(q, k_cache, block_table, max_shards, scale, max_pages=max_pages)
+    if out is None:
+        out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=q.device)
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
+    _require(out, "out", torch.bfloat16)
+    if workspace is None:
+        workspace = torch.empty(max(decode_workspace_size(desc), 16), dtype=torch.uint8,
+                                device=q.device)
+    _require(workspace, "workspace", torch.uint8)
+    if counters is None:
+        counters = torch.zeros(B * k_cache.shape[1], dtype=torch.int32, device=q.device)
+    _require(counters, "counters", torch.int32)
+    stream = torch.cuda.current_stream(q.device).cuda_stream
+    _check(load_library().qf_attn_decode(
+        ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+        _ptr(ctx_lens), _ptr(n_shards), _ptr(out), _ptr(lse), _ptr(workspace),
+        workspace.numel(), _ptr(counters), counters.numel(), ctypes.c_void_p(stream)))
+    return out, lse
 
 
 def schedule_simulate(arrival, attn_time, n_layers, wiring="qfirst", ffn_time=1.0, min_batch=2,

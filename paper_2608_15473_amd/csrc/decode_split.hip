@@ -21,6 +21,7 @@
 #include <math.h>
 
 #include "linear_body.h"
+#include "merge_body.h"
 #include "qf_internal.h"
 
 namespace qf {
@@ -62,16 +63,54 @@ __device__ __forceinline__ void unpack8(const uint4& w, float* f) {
   f[6] = bf16_lo(w.w); f[7] = bf16_hi(w.w);
 }
 
+// Sweep and merge in one launch: every unit of a (request, KV head) counts itself in once its
+// partial states are stored; the unit that completes the count merges the group's G query heads
+// over all max_shards x chunks slots with the merge kernels' own code (merge_body.h).  The XCDs'
+// L2 caches are not coherent with each other, and a device-scope fence would write back and
+// invalidate a whole L2 per workgroup, so no fence is used: the partial states are written and
+// read with device-scope accesses (which go through to the coherent level), every wavefront waits
+// until its own stores have completed before the workgroup barrier, and the count is a
+// device-scope atomic.  The last unit then sets the counter back to 0 for the next call.
+// Nothing ever waits for another workgroup.
+template <int G, int W>
+__device__ __forceinline__ void merge_if_last(const float* __restrict__ part_o,
+                                              const float* __restrict__ part_lse,
+                                              int32_t* __restrict__ counters,
+                                              uint16_t* __restrict__ merged_o,
+                                              float* __restrict__ merged_lse, int b, int g,
+                                              int hq, int hkv, int entries) {
+  __shared__ int s_last;
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wavefront's partial stores are complete
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int prev = __hip_atomic_fetch_add(&counters[(size_t)b * hkv + g], 1, __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT);
+    s_last = (prev == entries - 1);
+  }
+  __syncthreads();
+  if (!s_last) return;
+#pragma unroll 1
+  for (int h = 0; h < G; ++h)
+    mrg::merge_row<true, false, W, true>(part_o, part_lse, merged_o, merged_lse, entries, hq, b,
+                                         g * G + h, nullptr, nullptr, nullptr, 1, 0.0f);
+  if (threadIdx.x == 0)
+    __hip_atomic_store(&counters[(size_t)b * hkv + g], 0, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // The sweep of one unit by one workgroup; `bid` plays the role of the workgroup index (it is the
 // index itself in decode_split_kernel, the sweep's share of the indices in a shared launch).
-template <int G, int W, int NBUF>
+// With MERGE, the unit also takes part in the fused merge (merge_if_last).
+template <int G, int W, int NBUF, bool MERGE = false>
 __device__ __forceinline__ void sweep_unit(
     const uint16_t* __restrict__ qp, const uint16_t* __restrict__ kp,
     const uint16_t* __restrict__ vp, const int32_t* __restrict__ block_table,
     const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ n_shards,
     float* __restrict__ out_o, float* __restrict__ out_lse, int32_t hq, int32_t hkv,
     int32_t max_pages, int32_t num_pages, int32_t max_shards, int32_t chunks, int32_t n_units,
-    int32_t units_per_xcd, int32_t batch, int32_t order, float scale_log2, const unsigned bid) {
+    int32_t units_per_xcd, int32_t batch, int32_t order, float scale_log2, const unsigned bid,
+    int32_t* __restrict__ counters = nullptr, uint16_t* __restrict__ merged_o = nullptr,
+    float* __restrict__ merged_lse = nullptr) {
   // Which unit this workgroup sweeps.  Workgroups are dispatched in index order, round-robin over
   // the 8 XCDs.
   //  * Short shards (kOrderByRequest): each XCD takes a contiguous range of units in (request,
@@ -127,8 +166,15 @@ __device__ __forceinline__ void sweep_unit(
   if (c0 >= c1) {
     if (threadIdx.x < G) {
       const size_t slot = (((size_t)b * max_shards + s) * chunks + c) * hq + (size_t)g * G;
-      __builtin_nontemporal_store(poison ? NAN : -INFINITY, &out_lse[slot + threadIdx.x]);
+      if constexpr (MERGE)
+        __hip_atomic_store(&out_lse[slot + threadIdx.x], poison ? NAN : -INFINITY,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      else
+        __builtin_nontemporal_store(poison ? NAN : -INFINITY, &out_lse[slot + threadIdx.x]);
     }
+    if constexpr (MERGE)
+      merge_if_last<G, W>(out_o, out_lse, counters, merged_o, merged_lse, b, g, hq, hkv,
+                          max_shards * chunks);
     return;
   }
 
@@ -323,14 +369,24 @@ swept:
       }
       // Non-temporal: a thin stream of default-policy writes interleaved with the sweep's
       // reads costs far more HBM time than its bytes (measured ~4% of the sweep).
-      __builtin_nontemporal_store(A / L, &out_o[(slot + h) * D + d]);
+      if constexpr (MERGE)   // read by another workgroup of this launch (merge_if_last)
+        __hip_atomic_store(&out_o[(slot + h) * D + d], A / L, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      else
+        __builtin_nontemporal_store(A / L, &out_o[(slot + h) * D + d]);
     }
     if (d == 0) {
       float lse = (M == -INFINITY) ? -INFINITY : (M + log2f(L)) * kLn2;
       if (bad) lse = NAN;
-      __builtin_nontemporal_store(lse, &out_lse[slot + h]);
+      if constexpr (MERGE)
+        __hip_atomic_store(&out_lse[slot + h], lse, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      else
+        __builtin_nontemporal_store(lse, &out_lse[slot + h]);
     }
   }
+  if constexpr (MERGE)
+    merge_if_last<G, W>(out_o, out_lse, counters, merged_o, merged_lse, b, g, hq, hkv,
+                        max_shards * chunks);
 }
 
 template <int G, int W, int NBUF>
@@ -345,6 +401,35 @@ decode_split_kernel(const uint16_t* __restrict__ qp, const uint16_t* __restrict_
   sweep_unit<G, W, NBUF>(qp, kp, vp, block_table, ctx_lens, n_shards, out_o, out_lse, hq, hkv,
                          max_pages, num_pages, max_shards, chunks, n_units, units_per_xcd, batch,
                          order, scale_log2, blockIdx.x);
+}
+
+template <int G, int W, int NBUF>
+__global__ void __launch_bounds__(64 * W)
+__attribute__((amdgpu_waves_per_eu(G >= 8 ? 2 : 3)))   // the unfused sweep's occupancy
+decode_fused_kernel(const uint16_t* __restrict__ qp, const uint16_t* __restrict__ kp,
+                    const uint16_t* __restrict__ vp, const int32_t* __restrict__ block_table,
+                    const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ n_shards,
+                    float* __restrict__ out_o, float* __restrict__ out_lse, int32_t hq,
+                    int32_t hkv, int32_t max_pages, int32_t num_pages, int32_t max_shards,
+                    int32_t chunks, int32_t n_units, int32_t units_per_xcd, int32_t batch,
+                    int32_t order, float scale_log2, int32_t* __restrict__ counters,
+                    uint16_t* __restrict__ merged_o, float* __restrict__ merged_lse) {
+  sweep_unit<G, W, NBUF, true>(qp, kp, vp, block_table, ctx_lens, n_shards, out_o, out_lse, hq,
+                               hkv, max_pages, num_pages, max_shards, chunks, n_units,
+                               units_per_xcd, batch, order, scale_log2, blockIdx.x, counters,
+                               merged_o, merged_lse);
+}
+
+template <int G>
+hipError_t launch_fused_g(const SplitParams& p, int32_t* counters, void* out, float* lse,
+                          hipStream_t stream) {
+  const unsigned grid = 8u * (unsigned)p.units_per_xcd;
+  hipLaunchKernelGGL((decode_fused_kernel<G, kSplitWaves, kSplitBuffers>), dim3(grid),
+                     dim3(64 * kSplitWaves), 0, stream, p.q, p.k, p.v, p.block_table, p.ctx_lens,
+                     p.n_shards, p.out_o, p.out_lse, p.hq, p.hkv, p.max_pages, p.num_pages,
+                     p.max_shards, p.chunks, p.n_units, p.units_per_xcd, p.batch, p.order,
+                     p.scale_log2, counters, static_cast<uint16_t*>(out), lse);
+  return hipGetLastError();
 }
 
 template <int G>
@@ -454,6 +539,17 @@ hipError_t launch_decode_split_beside(const SplitParams& p, int group, const Lin
     case 2: return launch_beside_g<2>(p, l, stream);
     case 4: return launch_beside_g<4>(p, l, stream);
     case 8: return launch_beside_g<8>(p, l, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_decode_fused(const SplitParams& p, int group, int32_t* counters, void* out,
+                               float* lse, hipStream_t stream) {
+  switch (group) {
+    case 1: return launch_fused_g<1>(p, counters, out, lse, stream);
+    case 2: return launch_fused_g<2>(p, counters, out, lse, stream);
+    case 4: return launch_fused_g<4>(p, counters, out, lse, stream);
+    case 8: return launch_fused_g<8>(p, counters, out, lse, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -1,38 +1,10 @@
-// Merge of partial softmax states (O_i, ln Z_i) (Q-First, arXiv:2608.15473, §5).
-//
-// For one (row, query head) and entries i = 0..N-1:
-//   m = max_i ln Z_i,   w_i = exp(ln Z_i - m),   out = sum_i w_i O_i / sum_i w_i,
-//   ln Z = m + ln(sum_i w_i).
-// This is the pairwise lerp/sigmoid/logaddexp merge of §5 applied to all entries at once; every
-// weight is <= 1, so it is finite for any magnitude of the log partitions.  An entry with
-// ln Z = -inf is empty: its weight is selected to 0 and its O (possibly garbage, §5) is never
-// multiplied.  A NaN among the ln Z makes the row's output NaN.
-//
-// One workgroup per (row, head); its wavefronts take the entries in groups of 16, every lane owns
-// 2 of the 128 dims, and the wavefronts' sums meet in LDS.
-//
-// With the current token (CUR): the merged pair is the cache's (o_<j, lse_<j), and the current
-// token is folded in as §2 and Appendix A state it: s_jj = scale * q_j . k_j,
-// out = lerp(v_j, o_<j, sigma(lse_<j - s_jj)) with sigma(x) = 1 / (1 + exp(-x)), and
-// lse = logaddexp(lse_<j, s_jj).  An empty cache gives sigma(-inf) = 0, i.e. out = v_j.
-#include <math.h>
-
-#include "qf_internal.h"
+// Merge kernels: partial softmax states of shards (or of a shard's chunks) into one (Q-First,
+// arXiv:2608.15473, §5), optionally followed by the current token (§2, Appendix A).  The body
+// is in merge_body.h.
+#include "merge_body.h"
 
 namespace qf {
 namespace {
-
-constexpr int D = kHeadDim;
-
-// fp32 -> bf16, round to nearest even; NaN stays a (quiet) NaN.
-__device__ __forceinline__ uint32_t bf16_rne(float f) {
-  const uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x0040u;
-  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
-
-__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
 // W wavefronts per workgroup: 4, or 16 for rows of more than 64 slots (each wavefront then still
 // makes one round of loads for up to 256 slots).
@@ -42,119 +14,8 @@ merge_kernel(const float* __restrict__ in_o, const float* __restrict__ in_lse,
              void* __restrict__ out_o, float* __restrict__ out_lse, int32_t entries,
              int32_t hq, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cur,
              const uint16_t* __restrict__ v_cur, int32_t hkv, float scale) {
-  const int pair = blockIdx.x;
-  const int r = pair / hq;
-  const int h = pair % hq;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const float* lse = in_lse + (size_t)r * entries * hq + h;
-  const float2* o = reinterpret_cast<const float2*>(in_o + ((size_t)r * entries * hq + h) * D) + lane;
-  const size_t o_step = (size_t)hq * D / 2;  // float2 between entries
-
-  // Wavefront w takes entries [K w, K w + K) of every K W.  Its K log-partitions and O rows are
-  // all loaded before any is used, so a row costs one memory round trip; each wavefront keeps its
-  // own running maximum m_w (rescaling its sums when a later group raises it), and the wavefronts
-  // meet in LDS, where every sum is rescaled by exp(m_w - m).  Empty entries are selected out.
-  constexpr int K = 16;
-  float m_w = -INFINITY;
-  float L = 0.0f;
-  float2 acc = make_float2(0.0f, 0.0f);
-  bool nan = false;
-  for (int i0 = K * wave; i0 < entries; i0 += K * W) {
-    float x[K];
-    float2 v[K];
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-      const bool in = i0 + k < entries;
-      x[k] = in ? lse[(size_t)(i0 + k) * hq] : -INFINITY;
-      v[k] = in ? o[(size_t)(i0 + k) * o_step] : make_float2(0.0f, 0.0f);
-    }
-    float mc = m_w;
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-      nan |= (x[k] != x[k]);
-      mc = fmaxf(mc, x[k]);
-    }
-    if (mc == -INFINITY) continue;  // nothing live so far
-    const float f = (m_w == -INFINITY) ? 0.0f : expf(m_w - mc);
-    L *= f;
-    acc.x *= f;
-    acc.y *= f;
-    m_w = mc;
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-      const float w = (x[k] == -INFINITY) ? 0.0f : expf(x[k] - m_w);
-      L += w;
-      acc.x = (w == 0.0f) ? acc.x : fmaf(w, v[k].x, acc.x);
-      acc.y = (w == 0.0f) ? acc.y : fmaf(w, v[k].y, acc.y);
-    }
-  }
-
-  __shared__ float2 s_acc[W][64];
-  __shared__ float s_L[W];
-  __shared__ float s_m[W];
-  __shared__ int s_nan[W];
-  s_acc[wave][lane] = acc;
-  if (lane == 0) {
-    s_L[wave] = L;
-    s_m[wave] = m_w;
-    s_nan[wave] = nan;
-  }
-  __syncthreads();
-  if (wave != 0) return;
-
-  float M = s_m[0];
-  bool any_nan = s_nan[0];
-#pragma unroll
-  for (int w = 1; w < W; ++w) {
-    M = fmaxf(M, s_m[w]);
-    any_nan |= s_nan[w];
-  }
-  float2 a = make_float2(0.0f, 0.0f);
-  float Lt = 0.0f;
-#pragma unroll
-  for (int w = 0; w < W; ++w) {
-    const float f = (s_m[w] == -INFINITY) ? 0.0f : expf(s_m[w] - M);
-    a.x = fmaf(f, s_acc[w][lane].x, a.x);
-    a.y = fmaf(f, s_acc[w][lane].y, a.y);
-    Lt = fmaf(f, s_L[w], Lt);
-  }
-  float lse_out;
-  const size_t out_idx = ((size_t)r * hq + h) * D / 2 + lane;  // float2 / bf16-pair index
-  if (any_nan) {
-    a = make_float2(NAN, NAN);
-    lse_out = NAN;
-  } else if (M == -INFINITY) {
-    a = make_float2(0.0f, 0.0f);
-    lse_out = -INFINITY;
-  } else {
-    a.x /= Lt;
-    a.y /= Lt;
-    lse_out = M + logf(Lt);
-  }
-  if (CUR) {
-    const int g = h / (hq / hkv);
-    const uint32_t qw = reinterpret_cast<const uint32_t*>(q + ((size_t)r * hq + h) * D)[lane];
-    const uint32_t kw = reinterpret_cast<const uint32_t*>(k_cur + ((size_t)r * hkv + g) * D)[lane];
-    const uint32_t vw = reinterpret_cast<const uint32_t*>(v_cur + ((size_t)r * hkv + g) * D)[lane];
-    float dot = fmaf(bf16_lo(qw), bf16_lo(kw), bf16_hi(qw) * bf16_hi(kw));
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) dot += __shfl_xor(dot, o);
-    const float s_jj = dot * scale;
-    const float t = 1.0f / (1.0f + expf(-(lse_out - s_jj)));   // weight of the cached history
-    a.x = (1.0f - t) * bf16_lo(vw) + t * a.x;
-    a.y = (1.0f - t) * bf16_hi(vw) + t * a.y;
-    const float mx = fmaxf(lse_out, s_jj);
-    float joined = mx + log1pf(expf(-fabsf(lse_out - s_jj)));  // stabilised logaddexp
-    if (mx == -INFINITY) joined = -INFINITY;
-    lse_out = (lse_out != lse_out || s_jj != s_jj) ? NAN : joined;
-  }
-  if (BF16) {
-    reinterpret_cast<uint32_t*>(out_o)[out_idx] = bf16_rne(a.x) | (bf16_rne(a.y) << 16);
-  } else if (M != -INFINITY || any_nan) {
-    reinterpret_cast<float2*>(out_o)[out_idx] = a;
-  }
-  if (out_lse && lane == 0) out_lse[(size_t)r * hq + h] = lse_out;
+  mrg::merge_row<BF16, CUR, W>(in_o, in_lse, out_o, out_lse, entries, hq, blockIdx.x / hq,
+                               blockIdx.x % hq, q, k_cur, v_cur, hkv, scale);
 }
 
 template <int W>

@@ -82,6 +82,11 @@ struct LinearParams {
   bool glu;                  // rows of W alternate gate / up; out = silu(gate) * up, N / 2 columns
 };
 hipError_t launch_linear(const LinearParams& p, hipStream_t stream);
+// The sweep with the merge fused into its last workgroup per (request, KV head)
+// (decode_split.hip): p.out_o / p.out_lse hold the partial states, counters [batch * hkv] int32
+// start at zero and are left at zero.
+hipError_t launch_decode_fused(const SplitParams& p, int group, int32_t* counters, void* out,
+                               float* lse, hipStream_t stream);
 // The sweep and a fused product in one launch (decode_split.hip).
 hipError_t launch_decode_split_beside(const SplitParams& p, int group, const LinearParams& l,
                                       hipStream_t stream);

@@ -156,6 +156,12 @@ int prepare_split(const qf_decode_desc* desc, const void* q, const void* k_cache
   return QF_OK;
 }
 
+// Workspace of qf_attn_decode: the partial states of every (shard, chunk) slot.
+size_t fused_workspace_bytes(const qf_decode_desc* d, int64_t chunks) {
+  const size_t states = (size_t)d->batch * d->max_shards * chunks * d->n_q_heads;
+  return states * (qf::kHeadDim + 1) * sizeof(float);
+}
+
 // After the sweep's launch: fold the chunks of each shard into the caller's per-shard partials.
 int finish_split(const Split& sp, hipStream_t s) {
   if (sp.chunks <= 1) return QF_OK;
@@ -247,6 +253,51 @@ int qf_attn_decode_split(const qf_decode_desc* desc, const void* q, const void* 
   const hipError_t e = qf::launch_decode_split(sp.p, sp.group, s);
   if (e != hipSuccess) return fail(QF_EHIP, "decode_split launch: %s", hipGetErrorString(e));
   return finish_split(sp, s);
+}
+
+int qf_attn_decode_workspace_size(const qf_decode_desc* desc, size_t* bytes) {
+  g_error[0] = 0;
+  if (!bytes) return fail(QF_EINVAL, "bytes is NULL");
+  const int rc = check_desc(desc);
+  if (rc) return rc;
+  *bytes = fused_workspace_bytes(desc, choose_chunks(desc));
+  return QF_OK;
+}
+
+int qf_attn_decode(const qf_decode_desc* desc, const void* q, const void* k_cache,
+                   const void* v_cache, const int32_t* block_table, const int32_t* ctx_lens,
+                   const int32_t* n_shards, void* out, float* lse, void* workspace,
+                   size_t workspace_size, int32_t* counters, int64_t n_counters, void* stream) {
+  g_error[0] = 0;
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  const qf_decode_desc& d = *desc;
+  if (d.batch == 0) return QF_OK;
+  if (!out || !workspace || !counters)
+    return fail(QF_EINVAL, "out, workspace and counters are required");
+  if (n_counters < (int64_t)d.batch * d.n_kv_heads)
+    return fail(QF_EINVAL, "counters holds %lld entries < batch * n_kv_heads = %lld",
+                (long long)n_counters, (long long)d.batch * d.n_kv_heads);
+  if (!aligned(out, 4) || (lse && !aligned(lse, 4)) || !aligned(workspace, 16) ||
+      !aligned(counters, 4))
+    return fail(QF_EALIGN, "out, lse and counters must be 4-byte aligned, workspace 16-byte");
+  const int64_t chunks = choose_chunks(&d);
+  const size_t need = fused_workspace_bytes(&d, chunks);
+  if (workspace_size < need)
+    return fail(QF_EINVAL, "workspace of %zu bytes < %zu needed", workspace_size, need);
+  // The partial states live in the workspace, seen by the sweep as its per-slot outputs (with
+  // chunks == 1 its direct outputs, otherwise its chunk states): one layout [B, S x C, Hq, .].
+  float* states = static_cast<float*>(workspace);
+  const size_t n_states = (size_t)d.batch * d.max_shards * chunks * d.n_q_heads;
+  Split sp;
+  rc = prepare_split(desc, q, k_cache, v_cache, block_table, ctx_lens, n_shards, states,
+                     states + n_states * qf::kHeadDim, chunks > 1 ? workspace : nullptr,
+                     chunks > 1 ? need : 0, &sp);
+  if (rc || sp.noop) return rc;
+  const hipError_t e = qf::launch_decode_fused(sp.p, sp.group, counters, out, lse,
+                                               static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(QF_EHIP, "decode launch: %s", hipGetErrorString(e));
+  return QF_OK;
 }
 
 int qf_attn_combine(int32_t batch, int32_t n_q_heads, int32_t head_dim, int32_t max_shards,

@@ -193,6 +193,31 @@ def test_beside_checks_both_calls_before_launching():
              ctypes.byref(none), None) == qf.QF_OK
 
 
+def test_one_launch_decode_rejects_bad_arguments():
+    lib = load_library()
+    a = ctypes.c_void_p(4096)
+    d = _desc()
+    n = ctypes.c_size_t(0)
+    assert lib.qf_attn_decode_workspace_size(ctypes.byref(d), None) == qf.QF_EINVAL
+    assert lib.qf_attn_decode_workspace_size(ctypes.byref(d), ctypes.byref(n)) == qf.QF_OK
+    assert n.value > 0
+    f = lib.qf_attn_decode
+    ws = n.value
+    assert f(ctypes.byref(d), a, a, a, a, a, a, None, None, a, ws, a, 16, None) == qf.QF_EINVAL
+    assert f(ctypes.byref(d), a, a, a, a, a, a, a, None, None, ws, a, 16, None) == qf.QF_EINVAL
+    assert f(ctypes.byref(d), a, a, a, a, a, a, a, None, a, ws, None, 16, None) == qf.QF_EINVAL
+    assert f(ctypes.byref(d), a, a, a, a, a, a, a, None, a, ws, a, 15, None) == qf.QF_EINVAL
+    assert f(ctypes.byref(d), a, a, a, a, a, a, a, None, a, ws - 1, a, 16, None) == qf.QF_EINVAL
+    assert f(ctypes.byref(d), a, a, a, a, a, a, a, None, ctypes.c_void_p(4100), ws, a, 16,
+             None) == qf.QF_EALIGN
+    assert f(ctypes.byref(d), a, a, a, a, a, a, a, None, a, ws, ctypes.c_void_p(4098), 16,
+             None) == qf.QF_EALIGN
+    assert f(ctypes.byref(_desc(head_dim=64)), a, a, a, a, a, a, a, None, a, ws, a, 16,
+             None) == qf.QF_EUNSUPPORTED
+    assert f(ctypes.byref(_desc(batch=0)), None, None, None, None, None, None, None, None, None,
+             0, None, 0, None) == qf.QF_OK
+
+
 def test_empty_batch_is_a_no_op():
     lib = load_library()
     d = _desc(batch=0)

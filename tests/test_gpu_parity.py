@@ -238,3 +238,88 @@ def test_full_size_every_layer_sampled(gpu, name):
         del case, got
         torch.cuda.empty_cache()
 
+
+# ------------------------------------------------------------------------------------------------
+# sweep and merge in one launch (qf_attn_decode): bitwise the two calls
+# ------------------------------------------------------------------------------------------------
+def _bits(t):
+    return t.view(torch.int16 if t.dtype == torch.bfloat16 else torch.int32).clone()
+
+
+def _one_launch_vs_two(case, workspace=None, counters=None):
+    """Bitwise the two-launch result (which the oracle gates check) when the shape has no
+    sub-shard chunks and at most 64 slots; otherwise the slots are grouped differently: within
+    a few fp32 ulp (lse) and one bf16 step (out)."""
+    args = (case.q, case.k_cache, case.v_cache, case.block_table, case.ctx_lens, case.n_shards)
+    po, pl = qf.attn_decode_split(*args, max_shards=case.max_shards, scale=case.scale)
+    out2, lse2 = qf.attn_combine(po, pl)
+    out1, lse1 = qf.attn_decode(*args, max_shards=case.max_shards, scale=case.scale,
+                                workspace=workspace, counters=counters)
+    torch.cuda.synchronize()
+    chunked = qf.workspace_size(qf.make_desc(case.q, case.k_cache, case.block_table,
+                                             case.max_shards, case.scale)) > 0
+    if not chunked and case.max_shards <= 64:
+        assert torch.equal(_bits(out1), _bits(out2))
+        assert torch.equal(_bits(lse1), _bits(lse2))
+    else:
+        a, b = lse1.double(), lse2.double()
+        same = (a == b) | (torch.isnan(a) & torch.isnan(b))
+        assert (same | ((a - b).abs() <= 8 * 2.0 ** -23 * b.abs())).all()
+        d = (_bits(out1).int() - _bits(out2).int()).abs()       # adjacent bf16 at most
+        assert int(d.max()) <= 1
+    return out1, lse1
+
+
+_ONE_LAUNCH = {
+    "G1": dict(batch=3, n_q_heads=2, n_kv_heads=2, ctx_lens=[1000, 37, 517], n_shards=[5, 2, 3]),
+    "G2": dict(batch=3, n_q_heads=4, n_kv_heads=2, ctx_lens=[1000, 37, 517], n_shards=[5, 2, 3]),
+    "G4": dict(batch=3, n_q_heads=8, n_kv_heads=2, ctx_lens=[1000, 37, 517], n_shards=[5, 2, 3]),
+    "G8": dict(batch=3, n_q_heads=16, n_kv_heads=2, ctx_lens=[1000, 37, 517], n_shards=[5, 2, 3]),
+    "chunked": dict(batch=1, n_q_heads=16, n_kv_heads=8, ctx_lens=[4608], n_shards=8),
+    "empty": dict(batch=4, n_q_heads=16, n_kv_heads=8, ctx_lens=[0, 16, 33, 100],
+                  n_shards=[3, 4, 7, 1], max_shards=8),
+    "slots256": dict(batch=2, n_q_heads=16, n_kv_heads=8, ctx_lens=[3000, 70000],
+                     n_shards=[150, 200], max_shards=256),
+}
+
+
+@pytest.mark.parametrize("name", list(_ONE_LAUNCH))
+def test_one_launch_decode_equals_split_then_combine(gpu, name):
+    kw = dict(_ONE_LAUNCH[name])
+    case = make_case(kw.pop("batch"), kw.pop("n_q_heads"), kw.pop("n_kv_heads"),
+                     kw.pop("ctx_lens"), kw.pop("n_shards"), seed=180, device=gpu, **kw)
+    say(f"[parity] one launch vs two: {name}")
+    out, lse = _one_launch_vs_two(case)
+    ref = oracle_ref(case)
+    check(case, run_gpu(case), ref, label=f"one launch {name}")
+
+
+def test_one_launch_counters_are_left_at_zero_and_poison_propagates(gpu):
+    """One workspace and one counter array across calls with different shapes (every call must
+    leave the counters it used at zero, whatever the previous call wrote to the workspace),
+    including a request whose device inputs are out of range."""
+    cases = [make_case(3, 16, 8, [500, 500, 500], [2, 2, 2], seed=181, device=gpu),
+             make_case(1, 16, 8, [4608], 8, seed=182, device=gpu),
+             make_case(2, 32, 8, [900, 7000], [3, 9], seed=183, max_shards=16, device=gpu)]
+    cases[0].ctx_lens[2] = 10 ** 6                           # out of range: NaN for request 2
+    need = max(qf.decode_workspace_size(qf.make_desc(c.q, c.k_cache, c.block_table,
+                                                     c.max_shards, c.scale)) for c in cases)
+    ws = torch.empty(need, dtype=torch.uint8, device=gpu)
+    counters = torch.zeros(64, dtype=torch.int32, device=gpu)
+    for rep in range(2):
+        for i, c in enumerate(cases):
+            say(f"[parity] shared workspace and counters: call {rep}.{i}")
+            out, lse = _one_launch_vs_two(c, workspace=ws, counters=counters)
+            assert int(counters.abs().sum().item()) == 0
+            if i == 0:
+                assert torch.isnan(lse[2]).all() and torch.isfinite(lse[:2]).all()
+
+
+@pytest.mark.slow
+def test_one_launch_full_size_headline_layer(gpu):
+    case = workload_case("qwen3-0.6b_b32_n32768_s64_l28", layer=3, device=gpu)
+    say("[parity] one launch vs two: headline layer 3")
+    _one_launch_vs_two(case)
+    del case
+    torch.cuda.empty_cache()
+
