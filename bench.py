@@ -59,7 +59,7 @@ def algorithmic_bytes(case):
     return dict(kv=kv, sweep=sweep, combine=combine, attended=int(n.sum()))
 
 
-def committed_traffic(workload, two_launch=False):
+def committed_traffic(workload, two_launch=True):
     """HBM bytes per launch of the timed kernel (the one-launch sweep + merge, or the sweep of
     the two-launch step) from the committed rocprofv3 counter summary of this workload, or None
     when there is none or the kernel's sources changed since it was taken."""
