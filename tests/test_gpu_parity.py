@@ -323,3 +323,20 @@ def test_one_launch_full_size_headline_layer(gpu):
     del case
     torch.cuda.empty_cache()
 
+
+@pytest.mark.slow
+def test_maximum_sizes(gpu):
+    """The sweep's chunk cap (one unit of a 2^20-position cache: 1,024 chunks, merged into one
+    shard) and a large grid (4,096 requests of short contexts: 32,768 units), on sampled pairs."""
+    one = make_case(1, 1, 1, [1 << 20], 1, seed=190, device=gpu)
+    desc = qf.make_desc(one.q, one.k_cache, one.block_table, 1, one.scale)
+    assert qf.workspace_size(desc) == 1024 * 1 * (128 + 1) * 4      # 1,024 chunk states
+    _run(one, "one unit, 2^20 positions, 1024 chunks")
+    del one
+    n = np.random.default_rng(191).integers(0, 64, size=4096)
+    many = make_case(4096, 16, 8, n, 1, seed=192, device=gpu)
+    pairs = [(0, 0), (1000, 7), (2047, 15), (4095, 3)] + [(int(b), 5) for b in np.where(n == 0)[0][:2]]
+    _run(many, "4096 requests", pairs)
+    del many
+    torch.cuda.empty_cache()
+
