@@ -36,16 +36,17 @@ SHARDS = [3, 1, 1]
 SPARE = 8
 
 
-def _build(gpu, L=SHAPE.layers, seed=500):
+def _build(gpu, L=SHAPE.layers, seed=500, ctx=CTX, shards=SHARDS):
     Hq, Hkv = SHAPE.n_q_heads, SHAPE.n_kv_heads
     layers, caches = [], []
     for l in range(L):
         layers.append({k: t.to(gpu) for k, t in block_weights(SHAPE, seed + l).items()})
-        c = make_case(len(CTX), Hq, Hkv, CTX + SPARE, SHARDS, seed=seed + 100 + l, device=gpu)
+        c = make_case(len(ctx), Hq, Hkv, np.asarray(ctx) + SPARE, shards, seed=seed + 100 + l,
+                      device=gpu)
         c.ctx_lens -= SPARE
         caches.append(LayerCache(c.k_cache, c.v_cache, c.block_table, c.ctx_lens, c.n_shards))
-    stack = QFirstStack(layers, caches, Hq, Hkv, max_shards=max(SHARDS), scale=SCALE)
-    u = block_input(len(CTX), SHAPE.hidden, seed=seed + 999).to(gpu)
+    stack = QFirstStack(layers, caches, Hq, Hkv, max_shards=int(np.max(shards)), scale=SCALE)
+    u = block_input(len(ctx), SHAPE.hidden, seed=seed + 999).to(gpu)
     return stack, u
 
 
@@ -200,6 +201,25 @@ def test_all_modes_equal_the_serial_order_bitwise(gpu):
         assert _same_state(states["serial"], states[mode]), mode
     assert int(stack.status.item()) == 0
     assert stack.caches[0].ctx_lens.tolist() == (CTX + 2).tolist()
+
+
+def test_more_than_eight_requests_in_all_modes(gpu):
+    """Ten requests: every product runs in blocks of 8 rows and only the first block of
+    W_gate|W_up shares the sweep's launch; the three orders still agree bitwise."""
+    ctx = [300, 2, 0, 45, 1000, 17, 64, 5, 129, 700]
+    stack, u = _build(gpu, L=2, seed=650, ctx=ctx, shards=[3, 1, 1, 2, 4, 1, 1, 1, 2, 3])
+    saved = _state(stack)
+    ys, states = {}, {}
+    for mode in ("serial", "streams", "fused"):
+        say(f"[stage] ten requests, mode {mode}")
+        _restore(stack, saved)
+        ys[mode] = stack.step(u, mode=mode).clone()
+        torch.cuda.synchronize()
+        states[mode] = _state(stack)
+    for mode in ("streams", "fused"):
+        assert torch.equal(ys["serial"], ys[mode]), mode
+        assert _same_state(states["serial"], states[mode]), mode
+    assert torch.isfinite(ys["serial"].float()).all()
 
 
 @pytest.mark.parametrize("mode", ["fused", "streams", "serial"])
