@@ -1,8 +1,11 @@
 """MI355X (gfx950) split-KV grouped-query decode attention with an LSE shard merge.
 
 The computation is the cache-side sweep of the Q-First decode protocol (arXiv:2608.15473, §2 and
-§5); it runs in hand-written HIP kernels behind the C ABI of ``include/qfattn.h``
-(``lib/libqfattn.so``).  This package is the thin Python binding over that library.
+§5) with its merge, the current-token fold and cache append of the protocol (§2), the dense
+products of a decoder block and the sweep sharing a launch with the feed-forward (§3), and a
+simulation of the layer-wise decode schedule (Appendix D).  It all runs in hand-written HIP kernels
+behind the C ABI of ``include/qfattn.h`` (``lib/libqfattn.so``); this package is the thin Python
+binding over that library (``binding``) plus a stack of Q-First blocks built on it (``stage``).
 """
 
 from .binding import (  # noqa: F401
