@@ -432,14 +432,22 @@ hipError_t launch_fused_g(const SplitParams& p, int32_t* counters, void* out, fl
   return hipGetLastError();
 }
 
-template <int G>
-hipError_t launch_g(const SplitParams& p, hipStream_t stream) {
+template <int G, int NBUF>
+hipError_t launch_gn(const SplitParams& p, hipStream_t stream) {
   const unsigned grid = 8u * (unsigned)p.units_per_xcd;
-  hipLaunchKernelGGL((decode_split_kernel<G, kSplitWaves, kSplitBuffers>), dim3(grid), dim3(64 * kSplitWaves),
+  hipLaunchKernelGGL((decode_split_kernel<G, kSplitWaves, NBUF>), dim3(grid), dim3(64 * kSplitWaves),
                      0, stream, p.q, p.k, p.v, p.block_table, p.ctx_lens, p.n_shards, p.out_o,
                      p.out_lse, p.hq, p.hkv, p.max_pages, p.num_pages, p.max_shards, p.chunks,
                      p.n_units, p.units_per_xcd, p.batch, p.order, p.scale_log2);
   return hipGetLastError();
+}
+
+// Short shards are exactly those swept in request order (the host picks the order from the
+// shard length); NBUF only changes how far ahead pages are requested, never the arithmetic.
+template <int G>
+hipError_t launch_g(const SplitParams& p, hipStream_t stream) {
+  if (p.order == kOrderByRequest) return launch_gn<G, split_buffers_short(G)>(p, stream);
+  return launch_gn<G, kSplitBuffers>(p, stream);
 }
 
 // One launch, two roles: the sweep's workgroups and those of a fused product (linear_body.h) share

@@ -9,7 +9,13 @@ namespace qf {
 constexpr int kHeadDim = 128;     // D
 constexpr int kPage = 16;         // P
 constexpr int kSplitWaves = 4;    // waves per workgroup of the sweep kernel
-constexpr int kSplitBuffers = 2;  // pages in registers per wave (1 computed, the rest in flight)
+// Pages in registers per wave of the sweep (1 computed, the rest in flight).  Long shards keep
+// three wavefronts per SIMD with 2.  Short shards (a few pages per wavefront, so a workgroup's
+// life is mostly its first pages' latency) go deeper, at two wavefronts per SIMD: measured on
+// MI355X, 5 buffers make 32-page shards at G=2 2% faster, while long ragged shards lose 4% at
+// that occupancy.
+constexpr int kSplitBuffers = 2;
+constexpr int split_buffers_short(int group) { return group <= 2 ? 5 : group == 4 ? 3 : 2; }
 constexpr int kMergeWaves = 4;    // waves per workgroup of the merge kernel
 
 // Dispatch orders of the sweep's units (see decode_split.hip).
