@@ -63,21 +63,35 @@ def committed_traffic(workload, two_launch=True):
     """HBM bytes per launch of the timed kernel (the one-launch sweep + merge, or the sweep of
     the two-launch step) from the committed rocprofv3 counter summary of this workload, or None
     when there is none or the kernel's sources changed since it was taken."""
-    import hashlib
-
     kind = "decode_split" if two_launch else "decode_fused"
     path = os.path.join(ROOT, "profiles", f"{kind}_{workload}_hbm_traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
-    h = hashlib.sha256()
-    for name in ("decode_split.hip", "linear_body.h", "merge_body.h", "qf_internal.h"):
-        with open(os.path.join(ROOT, "paper_2608_15473_amd", "csrc", name), "rb") as f:
-            h.update(f.read())
-    if h.hexdigest() != rec.get("kernel_source_sha256"):
+    if kernel_source_digest() != rec.get("kernel_source_sha256"):
         return None
     return rec["traffic_bytes_per_launch"]
+
+
+KERNEL_SOURCES = ("decode_split.hip", "linear_body.h", "merge_body.h", "qf_internal.h")
+
+
+def kernel_source_digest():
+    """sha256 over the sweep's kernel sources with comments removed and white space collapsed, so
+    that committed counters stay attached to the code they measured and to nothing else."""
+    import hashlib
+    import re
+
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_15473_amd", "csrc", name)) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
+        h.update(b"\0")
+    return h.hexdigest()
 
 
 def cpu_baseline(cases, budget_s=15.0):

@@ -209,8 +209,8 @@ __device__ __forceinline__ void sweep_unit(
   // This wavefront's pages: c0 + wave + i * W for i < mine.
   const int mine = (c1 - c0 > wave) ? (c1 - c0 - wave + W - 1) / W : 0;
   auto page_of = [&](int i) { return c0 + wave + i * W; };
-  // Raw block-table entry of page i (read two pages ahead; checked only when used, so the scalar
-  // load's latency hides behind the page in flight).
+  // Raw block-table entry of page i (read one page past the last one in flight; checked only when
+  // used, so the scalar load's latency hides behind the pages in flight).
   auto entry = [&](int i) -> int {
     if (i >= mine) return 0;
     const int pg = page_of(i);
