@@ -74,7 +74,7 @@ def committed_traffic(workload, two_launch=True):
     return rec["traffic_bytes_per_launch"]
 
 
-KERNEL_SOURCES = ("decode_split.hip", "linear_body.h", "merge_body.h", "qf_internal.h")
+KERNEL_SOURCES = ("decode_split.hip", "merge.hip", "linear_body.h", "merge_body.h", "qf_internal.h")
 
 
 def kernel_source_digest():
