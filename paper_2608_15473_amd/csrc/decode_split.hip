@@ -241,13 +241,6 @@ __device__ __forceinline__ void sweep_unit(
 
   auto process = [&](uint4* kc, uint4* vc, int pg) {
     const int valid = n - pg * P;  // slots [0, valid) of this page are cached positions
-    if (valid < P) {
-      // Last, partial page: the slots past n hold no position.  Their values must not meet a
-      // zero weight (0 * NaN garbage = NaN), so clear them; their scores become -inf below.
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (4 * j + row >= valid) vc[j] = make_uint4(0u, 0u, 0u, 0u);
-    }
 
     // Scores of this row's 4 positions for the G heads, log2 domain.
     float sc[4][G];
@@ -285,6 +278,14 @@ __device__ __forceinline__ void sweep_unit(
     for (int j = 0; j < 4; ++j) {
       float vf[8];
       unpack8(vc[j], vf);
+      // Last, partial page: the slots past n hold no position.  Their values must not meet a
+      // zero weight (0 * NaN garbage = NaN), so the unpacked copies are cleared; their scores are
+      // -inf above.  (Clearing the page buffers themselves would make the compiler copy them and
+      // wait for the pages still in flight.)
+      if (valid < P && 4 * j + row >= valid) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) vf[e] = 0.0f;
+      }
 #pragma unroll
       for (int h = 0; h < G; ++h)
 #pragma unroll
