@@ -20,6 +20,8 @@
 // exceeds it by more than kLazy), so the O rescale is rare after a shard's first pages.
 #include <math.h>
 
+#include <atomic>
+
 #include "linear_body.h"
 #include "merge_body.h"
 #include "qf_internal.h"
@@ -529,7 +531,33 @@ hipError_t launch_beside_g(const SplitParams& p, const LinearParams& l, hipStrea
   }
 }
 
+template <int G>
+int resident_g() {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &per_cu, decode_split_kernel<G, kSplitWaves, kSplitBuffers>, 64 * kSplitWaves, 0) !=
+          hipSuccess) {
+    (void)hipGetLastError();  // leave no error behind for the next launch check
+    return 0;
+  }
+  return cus * per_cu;
+}
+
 }  // namespace
+
+int split_resident_workgroups(int group) {
+  static std::atomic<int> cached[4] = {{-1}, {-1}, {-1}, {-1}};
+  const int k = group == 1 ? 0 : group == 2 ? 1 : group == 4 ? 2 : group == 8 ? 3 : -1;
+  if (k < 0) return 0;
+  int v = cached[k].load(std::memory_order_relaxed);
+  if (v < 0) {
+    v = k == 0 ? resident_g<1>() : k == 1 ? resident_g<2>() : k == 2 ? resident_g<4>() : resident_g<8>();
+    if (v > 0) cached[k].store(v, std::memory_order_relaxed);
+  }
+  return v;
+}
 
 hipError_t launch_decode_split(const SplitParams& p, int group, hipStream_t stream) {
   switch (group) {

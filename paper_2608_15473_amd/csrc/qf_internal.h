@@ -104,6 +104,11 @@ int simulate_schedule(int R, const double* arrival, const double* attn_time, int
                       double* ffn_return);
 
 hipError_t launch_decode_split(const SplitParams& p, int group, hipStream_t stream);
+
+// Workgroups of the long-shard sweep (kSplitBuffers) at group size `group` that are resident on
+// the current device at once (compute units x workgroups per unit); 0 when there is no device to
+// ask.  Queried once per group size and kept.
+int split_resident_workgroups(int group);
 // to_bf16 = false: partial-state output (fp32 O not written for an empty row);
 // to_bf16 = true:  final output (bf16, +0 for an empty row).
 hipError_t launch_merge(const MergeParams& p, bool to_bf16, hipStream_t stream);

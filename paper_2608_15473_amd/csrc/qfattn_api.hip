@@ -24,9 +24,13 @@ int fail(int code, const char* fmt, ...) {
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
-// Target number of sweep workgroups: 8 per compute unit of an MI355X (256 CUs).  Depends on the
-// descriptor only, so a given shape always runs the same decomposition (and gives the same bits).
-constexpr int64_t kTargetWorkgroups = 2048;
+// Sub-shard chunks, only for shapes with fewer (request, shard, KV head) units than the sweep has
+// resident workgroups: as many chunks as fill one full set of resident workgroups, never a partial
+// second round (measured on the 1M-token shape, 128 units: 6 chunks beat 16 and 12).  The count
+// depends on the descriptor and the device's occupancy for the kernel only, so a given shape on a
+// given GPU always runs the same decomposition (and gives the same bits); with no device to ask
+// (a host without a GPU sizing a workspace) it assumes an MI355X at three workgroups per CU.
+constexpr int64_t kFallbackResident = 768;
 constexpr int64_t kMinPagesPerWave = 2;
 
 int check_desc(const qf_decode_desc* d) {
@@ -56,8 +60,11 @@ int check_desc(const qf_decode_desc* d) {
 int64_t choose_chunks(const qf_decode_desc* d) {
   const int64_t units = (int64_t)d->batch * d->n_kv_heads * d->max_shards;
   if (units <= 0) return 1;
+  int64_t slots = qf::split_resident_workgroups(d->n_q_heads / d->n_kv_heads);
+  if (slots <= 0) slots = kFallbackResident;
+  if (units >= slots) return 1;
   const int64_t est_pages = (d->max_pages_per_seq + d->max_shards - 1) / d->max_shards;
-  int64_t c = (kTargetWorkgroups + units - 1) / units;
+  int64_t c = slots / units;
   c = std::min(c, std::max<int64_t>(1, est_pages / (qf::kSplitWaves * kMinPagesPerWave)));
   return std::max<int64_t>(1, std::min<int64_t>(c, 1024));
 }
