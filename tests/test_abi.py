@@ -89,6 +89,29 @@ def test_workspace_only_when_units_are_few():
     assert n % 16 == 0
 
 
+def test_chunks_fill_one_set_of_resident_workgroups():
+    """Without a GPU to ask, the library assumes an MI355X at three sweep workgroups per CU (768):
+    the 1M-token shape's 128 units take 6 chunks (768 workgroups), whose states are
+    B * S * C * Hq * (128 + 1) fp32; a wavefront keeps at least 2 pages (C <= pages / 8), and
+    shapes with at least 768 units take none.  (On a GPU the count comes from its occupancy.)"""
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("the resident-workgroup count is the device's own here")
+
+    def chunks(**kw):
+        d = _desc(**kw)
+        rc, n = _ws(d)
+        assert rc == 0
+        per_chunk = d.batch * d.max_shards * d.n_q_heads * (128 + 1) * 4
+        assert n % per_chunk == 0
+        return n // per_chunk
+    assert chunks(batch=1, max_shards=16, max_pages_per_seq=65536, num_pages=65536) == 6
+    assert chunks(batch=1, max_shards=8, max_pages_per_seq=288, num_pages=288) == 4    # 36 pages
+    assert chunks(batch=3, max_shards=32, max_pages_per_seq=65536, num_pages=65536) == 0  # 768
+    assert chunks(batch=1, n_q_heads=1, n_kv_heads=1, max_shards=1,
+                  max_pages_per_seq=65536, num_pages=65536) == 768
+
+
 def test_null_and_misaligned_pointers_are_rejected_before_launch():
     lib = load_library()
     d = _desc()
