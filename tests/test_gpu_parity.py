@@ -99,6 +99,44 @@ def test_physical_page_placement_is_bitwise_irrelevant(gpu):
         assert np.array_equal(ga[key], gb[key], equal_nan=True), key
 
 
+@pytest.mark.parametrize("G", [2, 4])
+def test_garbage_past_the_last_position_is_never_used(gpu, G):
+    """The slots of a request's last page past its last position hold no position: NaN and Inf
+    there (in K and in V) must leave every result bitwise as it is with finite values there, in
+    the unchunked and chunked sweeps, both dispatch orders, and the one-launch decode."""
+    shapes = [  # (batch, ctx_lens, n_shards, max_shards)
+        (3, [1000, 37, 517], [5, 2, 3], None),          # short shards
+        (1, [4607], 8, None),                           # chunked, one request
+        (2, [70001, 9], [1, 1], None),                  # chunked, one long unit
+        # 768 units of at least 128 pages at full capacity: the long-shard order, unchunked
+        (24, [33001] + [997 * (k + 1) + 3 for k in range(23)], [16] + [1 + k % 4 for k in range(23)],
+         16),
+    ]
+    for i, (B, ctx, S, smax) in enumerate(shapes):
+        clean = make_case(B, 2 * G, 2, ctx, S, seed=300 + i, max_shards=smax, device=gpu)
+        dirty = make_case(B, 2 * G, 2, ctx, S, seed=300 + i, max_shards=smax, device=gpu)
+        bt = dirty.block_table.long()
+        for b in range(B):
+            n = int(dirty.ctx_lens[b])
+            if n % 16 == 0:
+                continue
+            last = int(bt[b, n // 16])
+            dirty.k_cache[last, :, n % 16:] = float("nan")
+            dirty.v_cache[last, :, n % 16:] = float("nan")
+            dirty.v_cache[last, :, 15] = float("inf")
+            dirty.k_cache[last, 0, 15] = float("-inf")
+        say(f"[parity] garbage past the last position: G={G} shape {i}")
+        ga, gb = run_gpu(clean), run_gpu(dirty)
+        for key in ("part_out", "part_lse", "out_bits", "lse"):
+            assert np.array_equal(ga[key], gb[key], equal_nan=True), (i, key)
+        args = lambda c: (c.q, c.k_cache, c.v_cache, c.block_table, c.ctx_lens, c.n_shards)
+        o1, l1 = qf.attn_decode(*args(clean), max_shards=clean.max_shards, scale=clean.scale)
+        o2, l2 = qf.attn_decode(*args(dirty), max_shards=dirty.max_shards, scale=dirty.scale)
+        torch.cuda.synchronize()
+        assert torch.equal(_bits(o1), _bits(o2)) and torch.equal(_bits(l1), _bits(l2)), i
+        assert bool(torch.isfinite(l2).all()), i
+
+
 def test_repeat_calls_are_deterministic(gpu):
     case = make_case(2, 32, 8, [3000, 1234], [6, 2], seed=150, device=gpu)
     g1, g2 = run_gpu(case), run_gpu(case)
