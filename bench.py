@@ -281,10 +281,11 @@ def stage_kernel_times(stack, u, w, shape, passes=2):
         "sweep + W_gate,W_up": sweep + lin(2 * I, H) - B * I * 2,    # writes the activation
         "W_down": lin(H, I, gain=False, res=True),
         "W_k,W_v": lin(2 * Hkv * D, H),
-        "merge + current-token fold": partials + B * Hq * D * 2 + 2 * B * Hkv * D * 2
-        + B * Hq * (D * 2 + 4),
+        # partials, q, k_j and v_j read; out and lse written; k_j and v_j written to the cache and
+        # ctx_lens read and advanced
+        "merge, current-token fold + cache append": partials + B * Hq * D * 2
+        + 2 * B * Hkv * D * 2 + B * Hq * (D * 2 + 4) + 2 * B * Hkv * D * 2 + 8 * B,
         "W_o": lin(H, Hq * D, gain=False, res=True),
-        "cache append": 4 * B * Hkv * D * 2 + 8 * B,
     }
     out = {}
     for name, ev in spans.items():

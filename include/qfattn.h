@@ -15,7 +15,7 @@
  * Entry points: the sweep and its merge (qf_attn_decode_split, qf_attn_combine, or both in one
  * launch: qf_attn_decode); the decode step
  * around them (qf_attn_combine_current folds in the current token, qf_kv_append writes it to the
- * cache); the dense products of a decoder block (qf_linear) and the sweep sharing one launch with
+ * cache, qf_attn_combine_current_append does both in one launch); the dense products of a decoder block (qf_linear) and the sweep sharing one launch with
  * one of them (qf_attn_decode_split_beside); and a host-side simulation of the layer-wise decode
  * schedule (qf_schedule_simulate).
  *
@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define QF_VERSION 2
+#define QF_VERSION 3
 
 #define QF_OK 0
 #define QF_EINVAL (-1)       /* null pointer, negative or inconsistent size, Hq % Hkv != 0   */
@@ -194,6 +194,27 @@ int qf_attn_combine_current(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads
 int qf_kv_append(const qf_decode_desc* desc, void* k_cache, void* v_cache,
                  const int32_t* block_table, int32_t* ctx_lens, const void* k_new,
                  const void* v_new, int32_t advance, int32_t* status, void* stream);
+
+/*
+ * qf_attn_combine_current and qf_kv_append (advance = 1) of the same current token in one launch:
+ * the merge with the current token answers the query (out, lse), and the current token's key and
+ * value are written at position n_b = ctx_lens[b] of every request, whose ctx_lens then becomes
+ * n_b + 1 (§2: the key and value follow the query into the cache once it has been answered).
+ * Results, cache contents, ctx_lens and status are exactly those of the two calls in sequence.
+ * The sweep that produced the partials must have been issued before (it never reads position n_b).
+ *
+ *   desc        batch, n_q_heads, n_kv_heads, head_dim, page_size, max_pages_per_seq, num_pages,
+ *               max_shards (the partials' slot count) and softmax_scale are used.
+ *   part_out, part_lse, q, out, lse       as for qf_attn_combine_current.
+ *   k_cur, v_cur                          the current token, as for qf_attn_combine_current; also
+ *                                         what is appended (k_new, v_new of qf_kv_append).
+ *   k_cache, v_cache, block_table, ctx_lens, status   as for qf_kv_append.
+ */
+int qf_attn_combine_current_append(const qf_decode_desc* desc, const float* part_out,
+                                   const float* part_lse, const void* q, const void* k_cur,
+                                   const void* v_cur, void* out, float* lse, void* k_cache,
+                                   void* v_cache, const int32_t* block_table, int32_t* ctx_lens,
+                                   int32_t* status, void* stream);
 
 /*
  * Host-side simulation of the layer-wise decode schedule (Appendix D, the wiring as a schedule).

@@ -25,6 +25,7 @@ from .binding import (  # noqa: F401
     QFError,
     attn_combine,
     attn_combine_current,
+    attn_combine_current_append,
     attn_decode,
     attn_decode_split,
     attn_decode_split_beside,

@@ -18,7 +18,8 @@ LIB_PATH = os.path.join(_HERE, "lib", "libqfattn.so")
 QF_OK, QF_EINVAL, QF_EUNSUPPORTED, QF_EALIGN, QF_EHIP = 0, -1, -2, -3, -4
 EXPORTED = ("qf_attn_decode_split_workspace_size", "qf_attn_decode_split", "qf_attn_combine",
             "qf_attn_decode_workspace_size", "qf_attn_decode",
-            "qf_attn_combine_current", "qf_kv_append", "qf_linear", "qf_attn_decode_split_beside",
+            "qf_attn_combine_current", "qf_attn_combine_current_append", "qf_kv_append",
+            "qf_linear", "qf_attn_decode_split_beside",
             "qf_schedule_simulate", "qf_last_error", "qf_version")
 QF_WIRING_QFIRST, QF_WIRING_COMPOSED = 0, 1
 QF_LINEAR_PLAIN, QF_LINEAR_RMS_NORM, QF_LINEAR_SWIGLU, QF_LINEAR_GLU_OUT = 0, 1, 2, 16
@@ -68,6 +69,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                    sz, vp, ctypes.c_int64, vp]
     lib.qf_attn_combine_current.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, vp,
                                             ctypes.c_float, vp, vp, vp]
+    lib.qf_attn_combine_current_append.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp,
+                                                   vp, vp, vp, vp, vp, vp, vp, vp]
     lib.qf_kv_append.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp, vp, i32, vp, vp]
     lib.qf_linear.argtypes = [i32, i32, i32, i32, vp, vp, vp, ctypes.c_float, vp, vp, i32, vp,
                               vp]
@@ -81,7 +84,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.qf_version.argtypes = []
     for name in ("qf_attn_decode_split_workspace_size", "qf_attn_decode_split",
                  "qf_attn_decode_workspace_size", "qf_attn_decode",
-                 "qf_attn_combine", "qf_attn_combine_current", "qf_kv_append",
+                 "qf_attn_combine", "qf_attn_combine_current", "qf_attn_combine_current_append",
+                 "qf_kv_append",
                  "qf_linear", "qf_attn_decode_split_beside", "qf_schedule_simulate", "qf_version"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
@@ -240,6 +244,46 @@ def attn_combine_current(part_out, part_lse, q, k_cur, v_cur, scale=None, out=No
     _check(load_library().qf_attn_combine_current(
         B, Hq, Hkv, D, S, _ptr(part_out), _ptr(part_lse), _ptr(q), _ptr(k_cur), _ptr(v_cur),
         float(scale), _ptr(out), _ptr(lse), ctypes.c_void_p(stream)))
+    return out, lse
+
+
+def attn_combine_current_append(part_out, part_lse, q, k_cur, v_cur, k_cache, v_cache, block_table,
+                                ctx_lens, scale=None, out=None, lse=None, status=None,
+                                max_pages=None):
+    """attn_combine_current, then kv_append of k_cur / v_cur with the context lengths advanced,
+    in one launch (qf_attn_combine_current_append); returns (out, lse)."""
+    _require(part_out, "part_out", torch.float32, 4)
+    _require(part_lse, "part_lse", torch.float32, 3)
+    _require(q, "q", torch.bfloat16, 3)
+    _require(k_cur, "k_cur", torch.bfloat16, 3)
+    _require(v_cur, "v_cur", torch.bfloat16, 3)
+    _require(k_cache, "k_cache", torch.bfloat16, 4)
+    _require(v_cache, "v_cache", torch.bfloat16, 4)
+    _require(ctx_lens, "ctx_lens", torch.int32, 1)
+    if block_table is not None:
+        _require(block_table, "block_table", torch.int32, 2)
+    if status is not None:
+        _require(status, "status", torch.int32)
+    B, S, Hq, D = part_out.shape
+    Hkv, P = k_cache.shape[1], k_cache.shape[2]
+    if (tuple(q.shape) != (B, Hq, D) or tuple(k_cur.shape) != (B, Hkv, D)
+            or v_cur.shape != k_cur.shape or v_cache.shape != k_cache.shape
+            or k_cache.shape[3] != D or ctx_lens.shape[0] != B):
+        raise QFError(QF_EINVAL, "q / k_cur / v_cur / cache / ctx_lens shapes do not match the partials")
+    if scale is None:
+        scale = D ** -0.5
+    if max_pages is None:
+        max_pages = block_table.shape[1] if block_table is not None else k_cache.shape[0] // max(B, 1)
+    if out is None:
+        out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=part_out.device)
+    if lse is None:
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=part_out.device)
+    desc = DecodeDesc(B, Hq, Hkv, D, P, int(max_pages), int(k_cache.shape[0]), S, float(scale))
+    stream = torch.cuda.current_stream(part_out.device).cuda_stream
+    _check(load_library().qf_attn_combine_current_append(
+        ctypes.byref(desc), _ptr(part_out), _ptr(part_lse), _ptr(q), _ptr(k_cur), _ptr(v_cur),
+        _ptr(out), _ptr(lse), _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(ctx_lens),
+        _ptr(status), ctypes.c_void_p(stream)))
     return out, lse
 
 

@@ -445,11 +445,11 @@ hipError_t launch_gn(const SplitParams& p, hipStream_t stream) {
   return hipGetLastError();
 }
 
-// Short shards are exactly those swept in request order (the host picks the order from the
-// shard length); NBUF only changes how far ahead pages are requested, never the arithmetic.
+// The host picks deep buffers from the shard length (short shards of at least kDeepMinPages);
+// NBUF only changes how far ahead pages are requested, never the arithmetic.
 template <int G>
 hipError_t launch_g(const SplitParams& p, hipStream_t stream) {
-  if (p.order == kOrderByRequest) return launch_gn<G, split_buffers_short(G)>(p, stream);
+  if (p.deep) return launch_gn<G, split_buffers_deep(G)>(p, stream);
   return launch_gn<G, kSplitBuffers>(p, stream);
 }
 

@@ -1,18 +1,9 @@
-// Paged cache append of the current token (Q-First, arXiv:2608.15473, §2: k_j and v_j follow the
-// query as a cache write nothing waits on).
-//
-// One workgroup per request b: n = ctx_lens[b] is the slot the current token takes; its page is
-// block_table[b, n / P] and its row n % P.  Each thread copies one bf16 pair of one KV head's key
-// and value (2 * Hkv * 128 values per request).  When asked, the context length is advanced by one
-// after every thread of the workgroup has read it, so no read can see the new value.  A position
-// past the table's capacity, or a page outside the pool, writes nothing and sets *status = 1.
-#include "qf_internal.h"
+// Paged cache append of the current token (Q-First, arXiv:2608.15473, §2): one workgroup per
+// request runs the append body of append_body.h.
+#include "append_body.h"
 
 namespace qf {
 namespace {
-
-constexpr int D = kHeadDim;
-constexpr int P = kPage;
 
 __global__ void __launch_bounds__(256)
 kv_append_kernel(uint16_t* __restrict__ k, uint16_t* __restrict__ v,
@@ -20,31 +11,8 @@ kv_append_kernel(uint16_t* __restrict__ k, uint16_t* __restrict__ v,
                  const uint16_t* __restrict__ k_new, const uint16_t* __restrict__ v_new,
                  int32_t* __restrict__ status, int32_t hkv, int32_t max_pages, int32_t num_pages,
                  int32_t advance) {
-  const int b = blockIdx.x;
-  const int n = ctx_lens[b];
-  bool ok = n >= 0 && n < max_pages * P;
-  int page = 0;
-  if (ok) {
-    page = block_table ? block_table[(size_t)b * max_pages + n / P] : b * max_pages + n / P;
-    ok = (unsigned)page < (unsigned)num_pages;
-  }
-  if (ok) {
-    const size_t row = ((size_t)page * hkv) * P * D + (size_t)(n % P) * D;  // head 0's row
-    for (int i = threadIdx.x; i < hkv * D / 2; i += blockDim.x) {
-      const int g = i / (D / 2);
-      const int e = i % (D / 2);
-      const size_t dst = row + (size_t)g * P * D;
-      const size_t src = ((size_t)b * hkv + g) * D;
-      reinterpret_cast<uint32_t*>(k + dst)[e] = reinterpret_cast<const uint32_t*>(k_new + src)[e];
-      reinterpret_cast<uint32_t*>(v + dst)[e] = reinterpret_cast<const uint32_t*>(v_new + src)[e];
-    }
-  } else if (status && threadIdx.x == 0) {
-    *status = 1;
-  }
-  if (advance) {
-    __syncthreads();  // every thread has read ctx_lens[b]
-    if (threadIdx.x == 0 && ok) ctx_lens[b] = n + 1;
-  }
+  app::append_request(k, v, block_table, ctx_lens, k_new, v_new, status, hkv, max_pages, num_pages,
+                      advance, blockIdx.x);
 }
 
 }  // namespace

@@ -1,6 +1,7 @@
 // Merge kernels: partial softmax states of shards (or of a shard's chunks) into one (Q-First,
 // arXiv:2608.15473, §5), optionally followed by the current token (§2, Appendix A).  The body
 // is in merge_body.h.
+#include "append_body.h"
 #include "merge_body.h"
 
 namespace qf {
@@ -18,8 +19,37 @@ merge_kernel(const float* __restrict__ in_o, const float* __restrict__ in_lse,
                                blockIdx.x % hq, q, k_cur, v_cur, hkv, scale);
 }
 
+// The merge with the current token, then the current token's cache append: the workgroup of
+// (request b, query head 0) also writes k_j and v_j of every KV head of b at position ctx_lens[b]
+// and advances it.  No other workgroup of the launch reads ctx_lens or the cache, and the sweep
+// that produced the partials never reads position ctx_lens[b], so the write races with nothing.
+template <int W>
+__global__ void __launch_bounds__(64 * W)
+merge_append_kernel(const float* __restrict__ in_o, const float* __restrict__ in_lse,
+                    void* __restrict__ out_o, float* __restrict__ out_lse, int32_t entries,
+                    int32_t hq, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cur,
+                    const uint16_t* __restrict__ v_cur, int32_t hkv, float scale,
+                    uint16_t* __restrict__ k_cache, uint16_t* __restrict__ v_cache,
+                    const int32_t* __restrict__ block_table, int32_t* __restrict__ ctx_lens,
+                    int32_t* __restrict__ status, int32_t max_pages, int32_t num_pages) {
+  const int b = blockIdx.x / hq, h = blockIdx.x % hq;
+  mrg::merge_row<true, true, W>(in_o, in_lse, out_o, out_lse, entries, hq, b, h, q, k_cur, v_cur,
+                                hkv, scale);
+  if (h == 0)
+    app::append_request(k_cache, v_cache, block_table, ctx_lens, k_cur, v_cur, status, hkv,
+                        max_pages, num_pages, 1, b);
+}
+
 template <int W>
 hipError_t launch_w(const MergeParams& p, bool to_bf16, unsigned grid, hipStream_t stream) {
+  if (p.append) {
+    const AppendParams& a = *p.append;
+    hipLaunchKernelGGL((merge_append_kernel<W>), dim3(grid), dim3(64 * W), 0, stream, p.in_o,
+                       p.in_lse, p.out_o, p.out_lse, p.entries, p.hq, p.q, p.k_cur, p.v_cur,
+                       p.hkv, p.scale, a.k, a.v, a.block_table, a.ctx_lens, a.status, a.max_pages,
+                       a.num_pages);
+    return hipGetLastError();
+  }
   if (p.q)
     hipLaunchKernelGGL((merge_kernel<true, true, W>), dim3(grid), dim3(64 * W), 0, stream, p.in_o,
                        p.in_lse, p.out_o, p.out_lse, p.entries, p.hq, p.q, p.k_cur, p.v_cur,

@@ -10,12 +10,14 @@ constexpr int kHeadDim = 128;     // D
 constexpr int kPage = 16;         // P
 constexpr int kSplitWaves = 4;    // waves per workgroup of the sweep kernel
 // Pages in registers per wave of the sweep (1 computed, the rest in flight).  Long shards keep
-// three wavefronts per SIMD with 2.  Short shards (a few pages per wavefront, so a workgroup's
-// life is mostly its first pages' latency) go deeper, at two wavefronts per SIMD: measured on
-// MI355X, 5 buffers make 32-page shards at G=2 2% faster, while long ragged shards lose 4% at
-// that occupancy.
+// three wavefronts per SIMD with 2.  Short shards of some length (a handful of pages per
+// wavefront, so a workgroup's life is mostly its first pages' latency) go deeper, at two
+// wavefronts per SIMD: measured on MI355X, 5 buffers make 32-page shards at G=2 2% faster, while
+// long ragged shards lose 4% at that occupancy and shards of 2-3 pages per wavefront lose up to
+// 19% (the occupancy is lost and the extra buffers stay empty).
 constexpr int kSplitBuffers = 2;
-constexpr int split_buffers_short(int group) { return group <= 2 ? 5 : group == 4 ? 3 : 2; }
+constexpr int split_buffers_deep(int group) { return group <= 2 ? 5 : group == 4 ? 3 : 2; }
+constexpr int kDeepMinPages = 4 * kSplitWaves;   // shard pages (at full capacity) for deep buffers
 constexpr int kMergeWaves = 4;    // waves per workgroup of the merge kernel
 
 // Dispatch orders of the sweep's units (see decode_split.hip).
@@ -39,6 +41,7 @@ struct SplitParams {
   int32_t n_units;              // B * max_shards * chunks * Hkv
   int32_t units_per_xcd;        // ceil(n_units / 8)
   int32_t order;                // kOrderByRequest or kOrderByShardDesc (dispatch order of units)
+  bool deep;                    // short shards of >= kDeepMinPages pages: split_buffers_deep(G)
   float scale_log2;             // softmax scale * log2(e)
 };
 
@@ -47,6 +50,8 @@ struct SplitParams {
 //   out O [rows, hq, D] (fp32 or bf16), lse [rows, hq] fp32 (may be null)
 // With q non-null (final output only) the current token is folded in after the merge:
 //   q bf16 [rows, hq, D], k_cur / v_cur bf16 [rows, hkv, D].
+struct AppendParams;
+
 struct MergeParams {
   const float* in_o;
   const float* in_lse;
@@ -58,6 +63,9 @@ struct MergeParams {
   const uint16_t* v_cur = nullptr;
   int32_t hkv = 1;
   float scale = 0.0f;
+  // With the current token (q, k_cur, v_cur): also append k_cur and v_cur to the cache and
+  // advance ctx_lens (AppendParams below; k_new / v_new / advance there are not used).
+  const AppendParams* append = nullptr;
 };
 
 // Cache append: write the current token's key and value at position ctx_lens[b] of request b.

@@ -145,6 +145,7 @@ int prepare_split(const qf_decode_desc* desc, const void* q, const void* k_cache
   // Short shards: short workgroups, prologue latency decides (keep a request on one XCD).
   const int64_t shard_pages = (d.max_pages_per_seq + d.max_shards - 1) / d.max_shards / chunks;
   p.order = shard_pages >= qf::kLongShardPages ? qf::kOrderByShardDesc : qf::kOrderByRequest;
+  p.deep = p.order == qf::kOrderByRequest && shard_pages >= qf::kDeepMinPages;
   p.scale_log2 = (float)((double)d.softmax_scale * 1.4426950408889634);
 
   sp->group = d.n_q_heads / d.n_kv_heads;
@@ -370,6 +371,58 @@ int qf_attn_combine_current(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads
   m.scale = softmax_scale;
   const hipError_t e = qf::launch_merge(m, true, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(QF_EHIP, "combine launch: %s", hipGetErrorString(e));
+  return QF_OK;
+}
+
+int qf_attn_combine_current_append(const qf_decode_desc* desc, const float* part_out,
+                                   const float* part_lse, const void* q, const void* k_cur,
+                                   const void* v_cur, void* out, float* lse, void* k_cache,
+                                   void* v_cache, const int32_t* block_table, int32_t* ctx_lens,
+                                   int32_t* status, void* stream) {
+  g_error[0] = 0;
+  const int rc = check_desc(desc);
+  if (rc) return rc;
+  const qf_decode_desc& d = *desc;
+  if (d.batch == 0) return QF_OK;
+  if (!part_out || !part_lse || !out || !q || !k_cur || !v_cur || !k_cache || !v_cache ||
+      !ctx_lens)
+    return fail(QF_EINVAL, "a required pointer is NULL");
+  if (!aligned(part_out, 16)) return fail(QF_EALIGN, "part_out must be 16-byte aligned");
+  if (!aligned(part_lse, 4) || !aligned(out, 4) || (lse && !aligned(lse, 4)) || !aligned(q, 4) ||
+      !aligned(k_cur, 4) || !aligned(v_cur, 4) || !aligned(k_cache, 4) || !aligned(v_cache, 4) ||
+      !aligned(ctx_lens, 4) || (block_table && !aligned(block_table, 4)) ||
+      (status && !aligned(status, 4)))
+    return fail(QF_EALIGN, "every pointer must be 4-byte aligned (part_out 16-byte)");
+  if (!block_table && (int64_t)d.batch * d.max_pages_per_seq > d.num_pages)
+    return fail(QF_EINVAL, "identity block table needs num_pages >= batch * max_pages_per_seq");
+  if ((int64_t)d.batch * d.n_q_heads > INT32_MAX) return fail(QF_EINVAL, "batch * n_q_heads too large");
+  qf::AppendParams a{};
+  a.k = static_cast<uint16_t*>(k_cache);
+  a.v = static_cast<uint16_t*>(v_cache);
+  a.block_table = block_table;
+  a.ctx_lens = ctx_lens;
+  a.status = status;
+  a.batch = d.batch;
+  a.hkv = d.n_kv_heads;
+  a.max_pages = d.max_pages_per_seq;
+  a.num_pages = d.num_pages;
+  a.advance = 1;
+  qf::MergeParams m{};
+  m.in_o = part_out;
+  m.in_lse = part_lse;
+  m.out_o = out;
+  m.out_lse = lse;
+  m.rows = d.batch;
+  m.entries = d.max_shards;
+  m.hq = d.n_q_heads;
+  m.q = static_cast<const uint16_t*>(q);
+  m.k_cur = static_cast<const uint16_t*>(k_cur);
+  m.v_cur = static_cast<const uint16_t*>(v_cur);
+  m.hkv = d.n_kv_heads;
+  m.scale = d.softmax_scale;
+  m.append = &a;
+  const hipError_t e = qf::launch_merge(m, true, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(QF_EHIP, "combine + append launch: %s", hipGetErrorString(e));
   return QF_OK;
 }
 

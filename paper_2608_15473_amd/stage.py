@@ -11,15 +11,15 @@ the two may run at once.  On one GPU this module offers three orders of the same
 
     main stream:       W_q N1(u) -> q --+--> SwiGLU(W_gate|W_up N2(u)) -> u + W_down(.) = z
                                         |     -> W_k|W_v N1(z) -> k, v --[join]--> merge + fold
-                                        |                              -> z + W_o attn = y; append
+                                        |                              + append -> z + W_o attn = y
     attention stream:                   +--> sweep of the layer's cache (split into shards) --^
 
   mode="fused":    the sweep and W_gate|W_up N2(u) in one launch whose workgroups take either
                    role (qf_attn_decode_split_beside), so the two share every CU.
 
 Every step is one of the library's HIP kernels: the four products fused with the normalisation
-or activation that feeds them and the residual add that follows (qf_linear), the sweep, the merge
-with the current-token fold, and the cache append.  All three modes produce bitwise identical
+or activation that feeds them and the residual add that follows (qf_linear), the sweep, and the merge
+with the current-token fold and the cache append in one launch.  All three modes produce bitwise identical
 outputs and caches.  Every buffer is allocated once, so a step can be captured in a HIP graph
 (``capture``).
 """
@@ -162,14 +162,13 @@ class QFirstStack:
                          out_b=self.v.view(B, -1))
         if mode == "streams":
             main.wait_stream(self.attn_stream)
-        with self._span("merge + current-token fold"):
-            qf.attn_combine_current(self.part_out, self.part_lse, self.q, self.k, self.v,
-                                    scale=self.scale, out=self.attn, lse=self.lse)
+        with self._span("merge, current-token fold + cache append"):    # one launch
+            qf.attn_combine_current_append(self.part_out, self.part_lse, self.q, self.k, self.v,
+                                           c.k_cache, c.v_cache, c.block_table, c.ctx_lens,
+                                           scale=self.scale, out=self.attn, lse=self.lse,
+                                           status=self.status)
         with self._span("W_o"):                                              # y = z + W_o attn
             self._linear(self.attn.view(B, -1), w["w_o"], out, residual=self.z)
-        with self._span("cache append"):
-            qf.kv_append(c.k_cache, c.v_cache, c.block_table, c.ctx_lens, self.k, self.v,
-                         advance=True, status=self.status)
         return out
 
     def step(self, u: torch.Tensor, mode: str = "fused") -> torch.Tensor:

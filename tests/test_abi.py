@@ -112,6 +112,30 @@ def test_chunks_fill_one_set_of_resident_workgroups():
                   max_pages_per_seq=65536, num_pages=65536) == 768
 
 
+def test_fold_and_append_rejects_before_launch():
+    """qf_attn_combine_current_append validates its descriptor and pointers on the host."""
+    lib = load_library()
+    a = ctypes.c_void_p(4096)
+    odd = ctypes.c_void_p(4096 + 2)
+    fn = lib.qf_attn_combine_current_append
+
+    def call(d, **over):
+        args = dict(po=a, pl=a, q=a, kc=a, vc=a, out=a, lse=None, kk=a, vv=a, bt=a, ctx=a,
+                    status=None)
+        args.update(over)
+        return fn(ctypes.byref(d), *args.values(), None)
+
+    assert call(_desc(n_q_heads=12)) == qf.QF_EINVAL
+    assert call(_desc(head_dim=64)) == qf.QF_EUNSUPPORTED
+    assert call(_desc(), kk=None) == qf.QF_EINVAL
+    assert call(_desc(), ctx=None) == qf.QF_EINVAL
+    assert call(_desc(), po=ctypes.c_void_p(4096 + 4)) == qf.QF_EALIGN
+    assert call(_desc(), vv=odd) == qf.QF_EALIGN
+    assert call(_desc(num_pages=1), bt=None) == qf.QF_EINVAL       # identity map out of the pool
+    assert call(_desc(batch=0)) == qf.QF_OK                        # nothing to do
+    assert load_library().qf_last_error().decode() == ""
+
+
 def test_null_and_misaligned_pointers_are_rejected_before_launch():
     lib = load_library()
     d = _desc()

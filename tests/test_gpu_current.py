@@ -154,3 +154,34 @@ def test_decode_step_then_append_is_consistent(gpu):
     torch.cuda.synchronize()
     np.testing.assert_allclose(lse2.cpu().numpy(), lse_fold, rtol=2e-6)
     np.testing.assert_allclose(out2.float().cpu().numpy(), out_fold, atol=1e-2 * 0.05, rtol=1e-2)
+
+
+@pytest.mark.parametrize("G", [1, 2, 4, 8])
+def test_fold_and_append_in_one_launch_equal_the_two_calls(gpu, G):
+    """qf_attn_combine_current_append: out, lse, both caches, ctx_lens and status bitwise those of
+    qf_attn_combine_current followed by qf_kv_append (advance), for empty, partial-page,
+    page-boundary and full requests (the full one is skipped and flagged), at every group size."""
+    ctx = [0, 15, 16, 33, 47]
+    a = _allocated_case(gpu, 5, 2 * G, 2, ctx, [1, 2, 1, 3, 2], seed=250 + G, max_pages=3)
+    a.ctx_lens[4] = 48                           # request 4 is full: three pages of 16
+    b = _allocated_case(gpu, 5, 2 * G, 2, ctx, [1, 2, 1, 3, 2], seed=250 + G, max_pages=3)
+    b.ctx_lens[4] = 48
+    k_new, v_new = _new_token(a, 260 + G)
+    po, pl = qf.attn_decode_split(a.q, a.k_cache, a.v_cache, a.block_table, a.ctx_lens,
+                                  a.n_shards, max_shards=a.max_shards, scale=a.scale)
+    say(f"[current] fold + append in one launch: G={G}")
+    sa = torch.zeros(1, dtype=torch.int32, device=gpu)
+    sb = torch.zeros(1, dtype=torch.int32, device=gpu)
+    out_a, lse_a = qf.attn_combine_current(po, pl, a.q, k_new, v_new, scale=a.scale)
+    qf.kv_append(a.k_cache, a.v_cache, a.block_table, a.ctx_lens, k_new, v_new, advance=True,
+                 status=sa)
+    out_b, lse_b = qf.attn_combine_current_append(po, pl, b.q, k_new, v_new, b.k_cache, b.v_cache,
+                                                  b.block_table, b.ctx_lens, scale=b.scale,
+                                                  status=sb)
+    torch.cuda.synchronize()
+    assert torch.equal(out_a.view(torch.int16), out_b.view(torch.int16))
+    assert torch.equal(lse_a.view(torch.int32), lse_b.view(torch.int32))
+    assert torch.equal(a.k_cache.view(torch.int16), b.k_cache.view(torch.int16))
+    assert torch.equal(a.v_cache.view(torch.int16), b.v_cache.view(torch.int16))
+    assert a.ctx_lens.tolist() == b.ctx_lens.tolist() == [1, 16, 17, 34, 48]
+    assert int(sa.item()) == int(sb.item()) == 1
