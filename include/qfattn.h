@@ -68,8 +68,10 @@ typedef struct qf_decode_desc {
 
 /*
  * Bytes of device workspace qf_attn_decode_split needs for this shape (0 is possible).  The
- * workspace holds partial states of sub-shard chunks when a shape has too few (request, KV head,
- * shard) units to fill the GPU.  Host-only; depends on the descriptor alone.
+ * workspace holds partial states of sub-shard chunks when a shape has fewer (request, KV head,
+ * shard) units than the sweep keeps resident on the GPU at once.  Host call; depends on the
+ * descriptor and on that resident count, which is queried from the current device once per
+ * process (an MI355X is assumed when there is no device), so query and launch agree.
  * Returns QF_OK, or QF_EINVAL / QF_EUNSUPPORTED for a descriptor qf_attn_decode_split rejects.
  */
 int qf_attn_decode_split_workspace_size(const qf_decode_desc* desc, size_t* bytes);
