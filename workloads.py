@@ -258,6 +258,10 @@ STAGE_WORKLOADS = {
         # otherwise make sub-shard chunks, so the current-token fold merges them directly.
         StageWorkload("qwen3-0.6b_stage_b1_n4608", 11, "qwen3-0.6b", batch=1, ctx=4608, shards=32),
         StageWorkload("qwen3-4b_stage_b1_n36480", 12, "qwen3-4b", batch=1, ctx=36480, shards=256),
+        # Eight requests (the products' row block): the sweep reads 8x the feed-forward's bytes.
+        # 16 shards per request (measured: shared launch 2.02 ms per step with 8, 1.99 with 16,
+        # 2.08 with 32).
+        StageWorkload("qwen3-0.6b_stage_b8_n4608", 13, "qwen3-0.6b", batch=8, ctx=4608, shards=16),
     ]
 }
 
