@@ -34,6 +34,21 @@ def test_group_sizes_ragged(gpu, G):
     _run(case, f"G={G} ragged")
 
 
+@pytest.mark.parametrize("G", [1, 2, 4, 8])
+def test_deep_buffers_ragged(gpu, G):
+    """The deep-buffer sweep (short shards of 16+ pages, no sub-shard chunks: NBUF 5 at G <= 2,
+    3 at G = 4) on ragged requests with partial last pages and shards of every length the split
+    rule gives, every output checked."""
+    rng = np.random.default_rng(190 + G)
+    ctx = rng.integers(1, 3001, size=48)
+    ctx[:4] = [3000, 16, 17, 255]
+    shards = rng.integers(1, 9, size=48)
+    case = make_case(48, 2 * G, 2, ctx, shards, seed=190 + G, max_shards=8, device=gpu)
+    assert qf.workspace_size(qf.make_desc(case.q, case.k_cache, case.block_table,
+                                          case.max_shards, case.scale)) == 0      # no chunks
+    _run(case, f"deep buffers G={G}")
+
+
 def test_empty_requests_and_more_shards_than_pages(gpu):
     case = make_case(4, 16, 8, [0, 16, 33, 100], [3, 4, 7, 1], seed=110, max_shards=8,
                      device=gpu)
