@@ -19,10 +19,11 @@ merge_kernel(const float* __restrict__ in_o, const float* __restrict__ in_lse,
                                blockIdx.x % hq, q, k_cur, v_cur, hkv, scale);
 }
 
-// The merge with the current token, then the current token's cache append: the workgroup of
-// (request b, query head 0) also writes k_j and v_j of every KV head of b at position ctx_lens[b]
-// and advances it.  No other workgroup of the launch reads ctx_lens or the cache, and the sweep
-// that produced the partials never reads position ctx_lens[b], so the write races with nothing.
+// The merge with the current token and the current token's cache append in one launch: the first
+// rows * hq workgroups merge (request b, query head h); each of the last `rows` workgroups writes
+// k_j and v_j of every KV head of its request at position ctx_lens[b] and advances it, at the same
+// time.  No other workgroup of the launch reads ctx_lens or the cache, and the sweep that produced
+// the partials never reads position ctx_lens[b], so the write races with nothing.
 template <int W>
 __global__ void __launch_bounds__(64 * W)
 merge_append_kernel(const float* __restrict__ in_o, const float* __restrict__ in_lse,
@@ -31,23 +32,25 @@ merge_append_kernel(const float* __restrict__ in_o, const float* __restrict__ in
                     const uint16_t* __restrict__ v_cur, int32_t hkv, float scale,
                     uint16_t* __restrict__ k_cache, uint16_t* __restrict__ v_cache,
                     const int32_t* __restrict__ block_table, int32_t* __restrict__ ctx_lens,
-                    int32_t* __restrict__ status, int32_t max_pages, int32_t num_pages) {
-  const int b = blockIdx.x / hq, h = blockIdx.x % hq;
-  mrg::merge_row<true, true, W>(in_o, in_lse, out_o, out_lse, entries, hq, b, h, q, k_cur, v_cur,
-                                hkv, scale);
-  if (h == 0)
+                    int32_t* __restrict__ status, int32_t max_pages, int32_t num_pages,
+                    int32_t merge_blocks) {
+  if ((int)blockIdx.x >= merge_blocks) {
     app::append_request(k_cache, v_cache, block_table, ctx_lens, k_cur, v_cur, status, hkv,
-                        max_pages, num_pages, 1, b);
+                        max_pages, num_pages, 1, (int)blockIdx.x - merge_blocks);
+    return;
+  }
+  mrg::merge_row<true, true, W>(in_o, in_lse, out_o, out_lse, entries, hq, blockIdx.x / hq,
+                                blockIdx.x % hq, q, k_cur, v_cur, hkv, scale);
 }
 
 template <int W>
 hipError_t launch_w(const MergeParams& p, bool to_bf16, unsigned grid, hipStream_t stream) {
   if (p.append) {
     const AppendParams& a = *p.append;
-    hipLaunchKernelGGL((merge_append_kernel<W>), dim3(grid), dim3(64 * W), 0, stream, p.in_o,
-                       p.in_lse, p.out_o, p.out_lse, p.entries, p.hq, p.q, p.k_cur, p.v_cur,
-                       p.hkv, p.scale, a.k, a.v, a.block_table, a.ctx_lens, a.status, a.max_pages,
-                       a.num_pages);
+    hipLaunchKernelGGL((merge_append_kernel<W>), dim3(grid + (unsigned)p.rows), dim3(64 * W), 0,
+                       stream, p.in_o, p.in_lse, p.out_o, p.out_lse, p.entries, p.hq, p.q, p.k_cur,
+                       p.v_cur, p.hkv, p.scale, a.k, a.v, a.block_table, a.ctx_lens, a.status,
+                       a.max_pages, a.num_pages, (int32_t)grid);
     return hipGetLastError();
   }
   if (p.q)

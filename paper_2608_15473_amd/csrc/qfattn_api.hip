@@ -395,7 +395,8 @@ int qf_attn_combine_current_append(const qf_decode_desc* desc, const float* part
     return fail(QF_EALIGN, "every pointer must be 4-byte aligned (part_out 16-byte)");
   if (!block_table && (int64_t)d.batch * d.max_pages_per_seq > d.num_pages)
     return fail(QF_EINVAL, "identity block table needs num_pages >= batch * max_pages_per_seq");
-  if ((int64_t)d.batch * d.n_q_heads > INT32_MAX) return fail(QF_EINVAL, "batch * n_q_heads too large");
+  if ((int64_t)d.batch * (d.n_q_heads + 1) > INT32_MAX)
+    return fail(QF_EINVAL, "batch * (n_q_heads + 1) too large");
   qf::AppendParams a{};
   a.k = static_cast<uint16_t*>(k_cache);
   a.v = static_cast<uint16_t*>(v_cache);
