@@ -29,6 +29,7 @@ from .binding import (  # noqa: F401
     attn_decode,
     attn_decode_split,
     attn_decode_split_beside,
+    DecodeStepPlan,
     decode_workspace_size,
     kv_append,
     load_library,

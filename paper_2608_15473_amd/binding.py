@@ -132,7 +132,8 @@ def workspace_size(desc: DecodeDesc) -> int:
 
 def _split_call(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards, scale,
                 part_out, part_lse, workspace, max_pages):
-    """Checks and allocations of qf_attn_decode_split: returns (C arguments, part_out, part_lse)."""
+    """Checks and allocations of qf_attn_decode_split: returns (C arguments, descriptor, part_out,
+    part_lse, workspace, n_shards), the last three as tensors the C arguments point into."""
     _require(q, "q", torch.bfloat16, 3)
     _require(k_cache, "k_cache", torch.bfloat16, 4)
     _require(v_cache, "v_cache", torch.bfloat16, 4)
@@ -166,7 +167,7 @@ def _split_call(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards
     args = (ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
             _ptr(ctx_lens), _ptr(n_shards), _ptr(part_out), _ptr(part_lse), _ptr(workspace),
             ws_bytes)
-    return args, desc, part_out, part_lse
+    return args, desc, part_out, part_lse, workspace, n_shards
 
 
 def attn_decode_split(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards=None,
@@ -178,9 +179,9 @@ def attn_decode_split(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_
     [B, max_pages] or None (identity); ctx_lens int32 [B]; n_shards an int or int32 [B].
     Returns (part_out fp32 [B, S_max, Hq, D], part_lse fp32 [B, S_max, Hq]).
     """
-    args, desc, part_out, part_lse = _split_call(q, k_cache, v_cache, block_table, ctx_lens,
-                                                 n_shards, max_shards, scale, part_out, part_lse,
-                                                 workspace, max_pages)
+    args, desc, part_out, part_lse, workspace, n_shards = _split_call(
+        q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards, scale, part_out,
+        part_lse, workspace, max_pages)
     stream = torch.cuda.current_stream(q.device).cuda_stream
     _check(load_library().qf_attn_decode_split(*args, ctypes.c_void_p(stream)))
     return part_out, part_lse
@@ -195,9 +196,9 @@ def attn_decode_split_beside(q, k_cache, v_cache, block_table, ctx_lens, n_shard
     keyword arguments (x, w, prologue, gain, eps, residual, out, split, out_b).  Returns
     (part_out, part_lse, the product's output(s)); bitwise the results of the two separate calls.
     """
-    args, desc, part_out, part_lse = _split_call(q, k_cache, v_cache, block_table, ctx_lens,
-                                                 n_shards, max_shards, scale, part_out, part_lse,
-                                                 workspace, max_pages)
+    args, desc, part_out, part_lse, workspace, n_shards = _split_call(
+        q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards, scale, part_out,
+        part_lse, workspace, max_pages)
     la, result = _linear_call(**beside)
     stream = torch.cuda.current_stream(q.device).cuda_stream
     _check(load_library().qf_attn_decode_split_beside(*args, ctypes.byref(la),
@@ -220,6 +221,65 @@ def attn_combine(part_out, part_lse, out=None, lse=None, want_lse=True):
     _check(load_library().qf_attn_combine(B, Hq, D, S, _ptr(part_out), _ptr(part_lse), _ptr(out),
                                           _ptr(lse), ctypes.c_void_p(stream)))
     return out, lse
+
+
+class DecodeStepPlan:
+    """attn_decode_split then attn_combine on fixed buffers, checked and converted once.
+
+    The arguments are those of ``attn_decode_split`` (plus ``out`` / ``lse`` of ``attn_combine``);
+    every tensor, the workspace included, is allocated here when not given and kept by the plan.
+    Calling the plan enqueues the two library calls on ``stream`` (default: the current stream at
+    construction) with the pointers taken at construction, so the caller updates tensors in
+    place (e.g. the query, the cache, ctx_lens) and never reallocates them; per call the host does
+    two foreign calls and nothing else, which matters when the kernels take a few microseconds.
+    Returns (out, lse).
+    """
+
+    def __init__(self, q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards=None,
+                 scale=None, part_out=None, part_lse=None, out=None, lse=None, workspace=None,
+                 max_pages=None, stream=None):
+        args, desc, part_out, part_lse, workspace, n_shards = _split_call(
+            q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards, scale, part_out,
+            part_lse, workspace, max_pages)
+        B, S, Hq, D = part_out.shape
+        if out is None:
+            out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=q.device)
+        if lse is None:
+            lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
+        _require(out, "out", torch.bfloat16, 3)
+        _require(lse, "lse", torch.float32, 2)
+        if tuple(out.shape) != (B, Hq, D) or tuple(lse.shape) != (B, Hq):
+            raise QFError(QF_EINVAL, "out / lse shapes do not match the partials")
+        if stream is None:
+            stream = torch.cuda.current_stream(q.device).cuda_stream
+        # keep every buffer (and the descriptor the first call points to) alive with the plan
+        self._keep = (q, k_cache, v_cache, block_table, ctx_lens, n_shards, part_out, part_lse,
+                      out, lse, workspace, desc)
+        self._desc = desc
+        lib = load_library()
+        self._split = lib.qf_attn_decode_split
+        self._combine = lib.qf_attn_combine
+        self._split_args = args + (ctypes.c_void_p(stream),)
+        self._combine_args = (B, Hq, D, S, _ptr(part_out), _ptr(part_lse), _ptr(out), _ptr(lse),
+                              ctypes.c_void_p(stream))
+        self.part_out, self.part_lse, self.out, self.lse = part_out, part_lse, out, lse
+
+    def split(self):
+        """Enqueue the sweep (qf_attn_decode_split) into part_out / part_lse."""
+        rc = self._split(*self._split_args)
+        if rc != QF_OK:
+            raise QFError(rc, load_library().qf_last_error().decode())
+
+    def combine(self):
+        """Enqueue the merge of the partials (qf_attn_combine) into out / lse."""
+        rc = self._combine(*self._combine_args)
+        if rc != QF_OK:
+            raise QFError(rc, load_library().qf_last_error().decode())
+
+    def __call__(self):
+        self.split()
+        self.combine()
+        return self.out, self.lse
 
 
 def attn_combine_current(part_out, part_lse, q, k_cur, v_cur, scale=None, out=None, lse=None):

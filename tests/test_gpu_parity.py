@@ -393,3 +393,29 @@ def test_maximum_sizes(gpu):
     del many
     torch.cuda.empty_cache()
 
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("many units", dict(batch=3, ctx_lens=[1000, 37, 517], n_shards=[5, 2, 3])),
+    ("chunked", dict(batch=1, ctx_lens=[4607], n_shards=8)),       # the plan owns a workspace
+])
+def test_decode_step_plan_equals_the_calls(gpu, name, kw):
+    """DecodeStepPlan: bitwise the two calls, after other allocations have come and gone (the
+    buffers it allocated are kept), and with its inputs changed in place between calls."""
+    import gc
+    case = make_case(kw["batch"], 16, 8, kw["ctx_lens"], kw["n_shards"], seed=330, device=gpu)
+    args = (case.q, case.k_cache, case.v_cache, case.block_table, case.ctx_lens, case.n_shards)
+    plan = qf.DecodeStepPlan(*args, max_shards=case.max_shards, scale=case.scale)
+    gc.collect()
+    junk = [torch.full((1 << 20,), float("nan"), device=gpu) for _ in range(8)]   # reuse bait
+    say(f"[parity] decode-step plan: {name}")
+    for _ in range(2):
+        out1, lse1 = plan()
+        out1, lse1 = out1.clone(), lse1.clone()
+        po, pl = qf.attn_decode_split(*args, max_shards=case.max_shards, scale=case.scale)
+        out2, lse2 = qf.attn_combine(po, pl)
+        torch.cuda.synchronize()
+        assert torch.equal(_bits(out1), _bits(out2)) and torch.equal(_bits(lse1), _bits(lse2))
+        case.ctx_lens[0] -= 5                                       # in place: the plan sees it
+        case.q.mul_(-1)
+    del junk
