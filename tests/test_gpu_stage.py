@@ -150,6 +150,7 @@ BESIDE_CASES = [  # (B, Hq, Hkv, ctx, shards, M, N, K, prologue, GLU output)
     (3, 8, 8, [300, 1, 77], 2, 8, 1002, 264, None, True),
     (2, 64, 8, [5000, 40], [6, 1], 3, 1024, 3072, "swiglu", False),
     (2, 16, 4, [128, 2048], 64, 2, 520, 1024, "rms_norm", False),  # unchunked: many units
+    (24, 16, 8, [3999], 4, 2, 1024, 1024, "rms_norm", False),      # the split call's deep buffers
 ]
 
 
