@@ -419,3 +419,50 @@ def test_decode_step_plan_equals_the_calls(gpu, name, kw):
         case.ctx_lens[0] -= 5                                       # in place: the plan sees it
         case.q.mul_(-1)
     del junk
+
+
+def test_position_sharding_over_two_sweeps(gpu):
+    """Position sharding as it would run over two devices (one GPU stands in for both): each
+    sweep sees only its half of every request's pages (its own block-table rows and context
+    length), the two sets of shard pairs are concatenated along the slot axis, and one combine
+    merges them (§5: any partition, any order). Gated against the oracle's unsplit attention and
+    within a few ulp of the one-sweep result."""
+    from parity import LSE_REL, PART_REL, bf16_neighbours
+    case = make_case(3, 16, 8, [5000, 3333, 17], [4, 3, 1], seed=340, device=gpu)
+    B, Hq, Hkv, D = case.shape
+    bt = case.block_table
+    ctx = case.ctx_lens.long()
+    pages = (ctx + 15) // 16
+    cut = pages // 2                                   # first device: pages [0, cut)
+    n1 = torch.minimum(cut * 16, ctx)
+    parts = []
+    for lo, n in ((torch.zeros_like(cut), n1), (cut, ctx - n1)):
+        rows = torch.full_like(bt, -1)
+        for b in range(B):
+            m = int((n[b] + 15) // 16)
+            rows[b, :m] = bt[b, int(lo[b]):int(lo[b]) + m]
+        po, pl = qf.attn_decode_split(case.q, case.k_cache, case.v_cache, rows,
+                                      n.to(torch.int32), 2, max_shards=2, scale=case.scale)
+        parts.append((po, pl))
+    po = torch.cat([parts[0][0], parts[1][0]], dim=1).contiguous()
+    pl = torch.cat([parts[0][1], parts[1][1]], dim=1).contiguous()
+    out2, lse2 = qf.attn_combine(po, pl)
+    po1, pl1 = qf.attn_decode_split(case.q, case.k_cache, case.v_cache, case.block_table,
+                                    case.ctx_lens, case.n_shards, max_shards=case.max_shards,
+                                    scale=case.scale)
+    out1, lse1 = qf.attn_combine(po1, pl1)
+    torch.cuda.synchronize()
+    say("[parity] position sharding over two sweeps")
+    ref = oracle_ref(case)
+    o2, l2 = out2.float().cpu().numpy(), lse2.cpu().numpy()
+    for b in range(B):
+        for h in range(Hq):
+            O, L = ref["out"][b, h], ref["lse"][b, h]
+            assert abs(l2[b, h] - L) <= LSE_REL * max(1.0, abs(L)), (b, h)
+            delta = PART_REL * float(np.max(np.abs(O)))
+            lo_, _ = bf16_neighbours(O - delta)
+            _, hi_ = bf16_neighbours(O + delta)
+            assert np.all((o2[b, h] >= lo_) & (o2[b, h] <= hi_)), (b, h)
+    a, c = lse1.double(), lse2.double()
+    assert ((a - c).abs() <= 8 * 2.0 ** -23 * a.abs()).all()
+    assert int((_bits(out1).int() - _bits(out2).int()).abs().max()) <= 1
