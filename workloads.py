@@ -254,10 +254,12 @@ class StageWorkload:
 STAGE_WORKLOADS = {
     w.name: w
     for w in [
-        # One request fills the GPU only when cut finely: as many shards as the sweep would
-        # otherwise make sub-shard chunks, so the current-token fold merges them directly.
-        StageWorkload("qwen3-0.6b_stage_b1_n4608", 11, "qwen3-0.6b", batch=1, ctx=4608, shards=32),
-        StageWorkload("qwen3-4b_stage_b1_n36480", 12, "qwen3-4b", batch=1, ctx=36480, shards=256),
+        # One request fills the GPU only when cut finely, so the shards do what sub-shard chunks
+        # would and the current-token fold merges them directly.  Measured (shared launch, one
+        # MI355X): 24 shards beat 32 at Qwen3-0.6B and 128 beat 256 at Qwen3-4B by 4% a step
+        # (fewer slots for the merge; 16 shards bring chunks and their merge launch back).
+        StageWorkload("qwen3-0.6b_stage_b1_n4608", 11, "qwen3-0.6b", batch=1, ctx=4608, shards=24),
+        StageWorkload("qwen3-4b_stage_b1_n36480", 12, "qwen3-4b", batch=1, ctx=36480, shards=128),
         # Eight requests (the products' row block): the sweep reads 8x the feed-forward's bytes.
         # 16 shards per request (measured: shared launch 2.02 ms per step with 8, 1.99 with 16,
         # 2.08 with 32).
