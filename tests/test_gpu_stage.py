@@ -74,6 +74,11 @@ LINEAR_CASES = [  # (M, N, K, prologue, residual, split)
     (4, 2048, 1024, "rms_norm", False, 1024),     # W_k|W_v into two buffers
     (7, 1001, 264, None, False, None),            # ragged: tail wavefront, partial chunk
     (8, 18, 4104, "rms_norm", True, 5),
+    # the matrix-core path (4+ rows, K a multiple of 32): ragged tiles, residual, split
+    (8, 1000, 1024, "rms_norm", True, None),
+    (6, 2048, 3072, None, True, None),
+    (4, 4096, 2560, "rms_norm", False, 2048),
+    (5, 17, 96, "rms_norm", False, 9),
 ]
 
 
@@ -113,7 +118,8 @@ def test_linear_matches_oracle(gpu, M, N, K, pro, res, split):
     assert ok.all(), (np.argwhere(~ok)[:4], out[~ok][:4], ref[~ok][:4])
 
 
-@pytest.mark.parametrize("M,I,K", [(1, 3072, 1024), (3, 9728, 2560), (8, 24, 520)])
+@pytest.mark.parametrize("M,I,K", [(1, 3072, 1024), (3, 9728, 2560), (8, 24, 520),
+                                   (8, 3072, 1024), (4, 52, 64)])
 def test_linear_glu_output_matches_oracle(gpu, M, I, K):
     """Rows of W alternating gate and up, output silu(gate) * up from the fp32 sums: within the
     bf16 values around the exact activation widened by the accumulation bounds of both sums
