@@ -14,10 +14,14 @@
 // 8c..8c+7 of position 4j + r.  Each row is an independent online-softmax sweeper over the
 // positions r, r+4, r+8, r+12 of every page; rows and wavefronts merge once, at the end.
 //
-// Per page and lane: QK^T with v_dot2c_f32_bf16 on the packed bf16 pairs (exact products, fp32
-// sums), a 16-lane DPP all-reduce per score, exp2 in the log2 domain, and fp32 FMAs for PV with
-// the bf16 values unpacked by shift/mask.  The running max is raised lazily (only when a score
-// exceeds it by more than kLazy), so the O rescale is rare after a shard's first pages.
+// Per page and lane, scores: at G = 4 query heads per KV head, on the matrix cores (the K tile
+// passes through LDS into the operand layout of four v_mfma_f32_16x16x32_bf16, which leave each
+// lane the scores of exactly the positions whose V it holds, for one head; the other heads' come
+// from the quad by DPP); otherwise with v_dot2c_f32_bf16 on the packed bf16 pairs and a 16-lane
+// DPP all-reduce per score.  Both take exact bf16 products and fp32 sums.  Then exp2 in the log2
+// domain and fp32 FMAs for PV with the bf16 values unpacked by shift/mask.  The running max is
+// raised lazily (only when a score exceeds it by more than kLazy), so the O rescale is rare after
+// a shard's first pages.
 #include <math.h>
 
 #include <atomic>
@@ -30,6 +34,8 @@ namespace qf {
 namespace {
 
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 
 constexpr int D = kHeadDim;
 constexpr int P = kPage;
@@ -49,6 +55,25 @@ __device__ __forceinline__ float row_sum16(float x) {
   x += __builtin_amdgcn_update_dpp(0.0f, x, 0x141, 0xF, 0xF, false);  // row_half_mirror
   x += __builtin_amdgcn_update_dpp(0.0f, x, 0x140, 0xF, 0xF, false);  // row_mirror
   return x;
+}
+
+// Lane 4*(c/4) + h's value in every lane c of its quad (DPP quad_perm [h,h,h,h]).
+__device__ __forceinline__ float quad_bcast(float x, int h) {
+  const int v = __float_as_int(x);
+  switch (h) {
+    case 0: return __int_as_float(__builtin_amdgcn_mov_dpp(v, 0x00, 0xF, 0xF, true));
+    case 1: return __int_as_float(__builtin_amdgcn_mov_dpp(v, 0x55, 0xF, 0xF, true));
+    case 2: return __int_as_float(__builtin_amdgcn_mov_dpp(v, 0xAA, 0xF, 0xF, true));
+    default: return __int_as_float(__builtin_amdgcn_mov_dpp(v, 0xFF, 0xF, 0xF, true));
+  }
+}
+
+// 16-byte slot of chunk `ch` (dims 8ch..8ch+7) of position `pos` in a wavefront's 4 KB K tile in
+// LDS.  The XOR swizzle makes both the row-wise writes and the column-wise operand reads free of
+// bank conflicts: a position's 16 chunks stay in its 256 bytes, and the 16 positions read together
+// for one chunk land in 16 different slots of their rows.
+__device__ __forceinline__ int kslot(int pos, int ch) {
+  return pos * 16 + (ch ^ (4 * (pos & 3) + (pos >> 2)));
 }
 
 // Block-table entries are wave-uniform: read them through the constant address space so they
@@ -185,15 +210,35 @@ __device__ __forceinline__ void sweep_unit(
   const int row = lane >> 4;
   const int col = lane & 15;
 
-  // Queries of the group, dims 8col..8col+7, as packed bf16 pairs.
+  // With 4 heads per KV head the scores come from the matrix cores (process_mf below); otherwise
+  // the VALU computes them (process_valu).  Measured: the matrix path is 1-5% faster at G = 4,
+  // where the VALU path spends most of its issue slots on the dot products and reductions, and
+  // 1-2.5% slower at G = 2, where the VALU has slack and the LDS round trip only adds latency.
+  constexpr bool MF = G == 4;
+
+  // Queries of the group.  VALU path: dims 8col..8col+7 of every head as packed bf16 pairs.
+  // Matrix path: the queries are the 16 columns of the B operand of S^T = K Q^T (column c holds
+  // head c % G), split over the dims in 4 steps of 32: lane (row, col) holds dims
+  // 32kk + 8row .. 32kk + 8row + 7 of head col % G for step kk.
   uint32_t qv[G][4];
+  bf16x8_t qb[4];
+  if constexpr (MF) {
+    const uint4* qrow = reinterpret_cast<const uint4*>(qp + ((size_t)b * hq + (size_t)g * G + col % G) * D);
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
-    const uint4 t = reinterpret_cast<const uint4*>(qp + ((size_t)b * hq + (size_t)g * G + h) * D)[col];
-    qv[h][0] = t.x; qv[h][1] = t.y; qv[h][2] = t.z; qv[h][3] = t.w;
+    for (int kk = 0; kk < 4; ++kk) qb[kk] = __builtin_bit_cast(bf16x8_t, qrow[4 * kk + row]);
+  } else {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const uint4 t = reinterpret_cast<const uint4*>(qp + ((size_t)b * hq + (size_t)g * G + h) * D)[col];
+      qv[h][0] = t.x; qv[h][1] = t.y; qv[h][2] = t.z; qv[h][3] = t.w;
+    }
   }
 
+  // Online-softmax state.  VALU path: every lane keeps (m, l) of all G heads for its row.  Matrix
+  // path: lane (row, col) keeps them for head col % G only (m1, l1); the other heads' values sit
+  // in the same quad and are broadcast when needed.  acc: dims 8col..8col+7 of every head.
   float m[G], l[G], acc[G][8];
+  float m1 = -INFINITY, l1 = 0.0f;
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     m[h] = -INFINITY;
@@ -241,7 +286,86 @@ __device__ __forceinline__ void sweep_unit(
       vv[j] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, lane * 16, j * 1024, kNonTemporal));
   };
 
-  auto process = [&](uint4* kc, uint4* vc, int pg) {
+  // P V for the 4 positions of this row, weights pr[j][h] of position 4j + row.
+  auto accumulate = [&](uint4* vc, int valid, auto&& weight) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float vf[8];
+      unpack8(vc[j], vf);
+      // Last, partial page: the slots past n hold no position.  Their values must not meet a
+      // zero weight (0 * NaN garbage = NaN), so the unpacked copies are cleared; their scores are
+      // -inf.  (Clearing the page buffers themselves would make the compiler copy them and wait
+      // for the pages still in flight.)
+      if (valid < P && 4 * j + row >= valid) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) vf[e] = 0.0f;
+      }
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float p = weight(j, h);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(p, vf[e], acc[h][e]);
+      }
+    }
+  };
+
+  // Matrix path.  The page's K tile goes through this wavefront's 4 KB of LDS: the coalesced
+  // loads give lane (row, col) dims 8col.. of position 4j + row, and the operand reads give lane
+  // (row, col) dims 32kk + 8row.. of position pi(col) = 4(col % 4) + col / 4, so that the
+  // 16 x 16 result S^T = K Q^T lands with lane (row, col) holding the scores of positions
+  // 4i + row (i = 0..3), the very positions whose V this lane reads, for head col % G.  Four
+  // v_mfma_f32_16x16x32_bf16 (exact bf16 products, fp32 sums) replace 4G dot products and 4G
+  // 16-lane reductions per position quad.
+  __shared__ uint4 s_k[MF ? W : 1][MF ? P * 16 : 1];
+  auto process_mf = [&](uint4* kc, uint4* vc, int pg) {
+    const int valid = n - pg * P;  // slots [0, valid) of this page are cached positions
+    uint4* tile = s_k[wave];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) tile[kslot(4 * j + row, col)] = kc[j];
+    // LDS operations of one wavefront complete in order; the fence only keeps the compiler from
+    // moving the operand reads above the writes of other lanes' slots.
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    const int pos = 4 * (col & 3) + (col >> 2);
+    f32x4_t st = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+      st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+          __builtin_bit_cast(bf16x8_t, tile[kslot(pos, 4 * kk + row)]), qb[kk], st, 0, 0, 0);
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+
+    float sc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sc[i] = st[i] * scale_log2;
+    if (valid < P) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (4 * i + row >= valid) sc[i] = -INFINITY;
+    }
+    const float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
+    const bool raise = mx > m1 + kLazy;
+    float alpha = 1.0f;
+    if (raise) {
+      alpha = __builtin_amdgcn_exp2f(m1 - mx);  // m1 = -inf -> 0
+      l1 *= alpha;
+      m1 = mx;
+    }
+    if (__builtin_amdgcn_ballot_w64(raise)) {   // rare after a shard's first page
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float a = G == 1 ? alpha : quad_bcast(alpha, h);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[h][e] *= a;
+      }
+    }
+    const float base = (m1 == -INFINITY) ? 0.0f : m1;
+    float pr[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pr[i] = __builtin_amdgcn_exp2f(sc[i] - base);
+    l1 += (pr[0] + pr[1]) + (pr[2] + pr[3]);
+    accumulate(vc, valid, [&](int j, int h) { return G == 1 ? pr[j] : quad_bcast(pr[j], h); });
+  };
+
+  auto process_valu = [&](uint4* kc, uint4* vc, int pg) {
     const int valid = n - pg * P;  // slots [0, valid) of this page are cached positions
 
     // Scores of this row's 4 positions for the G heads, log2 domain.
@@ -275,24 +399,7 @@ __device__ __forceinline__ void sweep_unit(
       for (int j = 0; j < 4; ++j) pr[j][h] = __builtin_amdgcn_exp2f(sc[j][h] - base);
       l[h] += (pr[0][h] + pr[1][h]) + (pr[2][h] + pr[3][h]);
     }
-
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      float vf[8];
-      unpack8(vc[j], vf);
-      // Last, partial page: the slots past n hold no position.  Their values must not meet a
-      // zero weight (0 * NaN garbage = NaN), so the unpacked copies are cleared; their scores are
-      // -inf above.  (Clearing the page buffers themselves would make the compiler copy them and
-      // wait for the pages still in flight.)
-      if (valid < P && 4 * j + row >= valid) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) vf[e] = 0.0f;
-      }
-#pragma unroll
-      for (int h = 0; h < G; ++h)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pr[j][h], vf[e], acc[h][e]);
-    }
+    accumulate(vc, valid, [&](int j, int h) { return pr[j][h]; });
   };
 
   // Rotation over NBUF register buffers: pages i+1 .. i+NBUF-1 stream in while page i is
@@ -314,10 +421,20 @@ __device__ __forceinline__ void sweep_unit(
       issue(kbuf[(t + NBUF - 1) % NBUF], vbuf[(t + NBUF - 1) % NBUF], ph_next, ahead < mine);
       ph_next = entry(ahead + 1);
       if (i + t >= mine) goto swept;
-      process(kbuf[t], vbuf[t], page_of(i + t));
+      if constexpr (MF)
+        process_mf(kbuf[t], vbuf[t], page_of(i + t));
+      else
+        process_valu(kbuf[t], vbuf[t], page_of(i + t));
     }
   }
 swept:
+  if constexpr (MF) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      m[h] = G == 1 ? m1 : quad_bcast(m1, h);
+      l[h] = G == 1 ? l1 : quad_bcast(l1, h);
+    }
+  }
 
   // Merge the 4 rows of the wavefront (lanes col, col+16, col+32, col+48 hold the same dims).
 #pragma unroll
@@ -392,8 +509,11 @@ swept:
                         max_shards * chunks);
 }
 
+// Three wavefronts per SIMD with two page buffers (the long-shard sweep): the matrix path at G = 4
+// needs the hint to stay within 168 registers (it does, without spills); deeper buffers take two.
 template <int G, int W, int NBUF>
 __global__ void __launch_bounds__(64 * W)
+__attribute__((amdgpu_waves_per_eu(NBUF == 2 && G <= 4 ? 3 : 2)))
 decode_split_kernel(const uint16_t* __restrict__ qp, const uint16_t* __restrict__ kp,
                     const uint16_t* __restrict__ vp, const int32_t* __restrict__ block_table,
                     const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ n_shards,
