@@ -263,17 +263,21 @@ __device__ __forceinline__ void sweep_unit(
     const int pg = page_of(i);
     return bt ? bt[pg] : b * max_pages + pg;
   };
-  // One 4 KB page of one KV head through a buffer resource: a resource of size 0 (no page) turns
-  // the loads into no-ops that return zeros, so the prefetch below is unconditional and the
-  // wait counts stay static.  The loads are non-temporal (cache policy nt): every cached byte
-  // is read exactly once per sweep, and on gfx950 streaming reads marked nt reach a markedly
-  // higher share of HBM bandwidth than default-policy reads.
-  auto issue = [&](uint4* kk, uint4* vv, int ph, bool live) {
+  // One 4 KB page of one KV head through a buffer resource whose size covers the page's cached
+  // positions only: loads past it return zeros, so a page that does not exist (size 0) costs no
+  // traffic and keeps the prefetch below unconditional and the wait counts static, and the slots
+  // past the last position of a partial page read as zeros instead of whatever the pool holds
+  // there (a zero V meets a zero weight; the scores of those slots are set to -inf).  The loads
+  // are non-temporal (cache policy nt): every cached byte is read exactly once per sweep, and on
+  // gfx950 streaming reads marked nt reach a markedly higher share of HBM bandwidth than
+  // default-policy reads.
+  auto issue = [&](uint4* kk, uint4* vv, int ph, int i) {
+    const bool live = i < mine;
     if ((unsigned)ph >= (unsigned)num_pages) {
       poison |= live;
       ph = 0;
     }
-    const int bytes = live ? P * D * 2 : 0;
+    const int bytes = live ? min(n - page_of(i) * P, P) * D * 2 : 0;
     const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t*>(kbase + (size_t)ph * page_stride), (short)0, bytes, 0x00020000);
     const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
@@ -286,20 +290,13 @@ __device__ __forceinline__ void sweep_unit(
       vv[j] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, lane * 16, j * 1024, kNonTemporal));
   };
 
-  // P V for the 4 positions of this row, weights pr[j][h] of position 4j + row.
-  auto accumulate = [&](uint4* vc, int valid, auto&& weight) {
+  // P V for the 4 positions of this row, weights pr[j][h] of position 4j + row.  (The slots past
+  // the last position of a partial page were loaded as zeros and have zero weights.)
+  auto accumulate = [&](uint4* vc, auto&& weight) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       float vf[8];
       unpack8(vc[j], vf);
-      // Last, partial page: the slots past n hold no position.  Their values must not meet a
-      // zero weight (0 * NaN garbage = NaN), so the unpacked copies are cleared; their scores are
-      // -inf.  (Clearing the page buffers themselves would make the compiler copy them and wait
-      // for the pages still in flight.)
-      if (valid < P && 4 * j + row >= valid) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) vf[e] = 0.0f;
-      }
 #pragma unroll
       for (int h = 0; h < G; ++h) {
         const float p = weight(j, h);
@@ -362,7 +359,7 @@ __device__ __forceinline__ void sweep_unit(
 #pragma unroll
     for (int i = 0; i < 4; ++i) pr[i] = __builtin_amdgcn_exp2f(sc[i] - base);
     l1 += (pr[0] + pr[1]) + (pr[2] + pr[3]);
-    accumulate(vc, valid, [&](int j, int h) { return G == 1 ? pr[j] : quad_bcast(pr[j], h); });
+    accumulate(vc, [&](int j, int h) { return G == 1 ? pr[j] : quad_bcast(pr[j], h); });
   };
 
   auto process_valu = [&](uint4* kc, uint4* vc, int pg) {
@@ -378,9 +375,16 @@ __device__ __forceinline__ void sweep_unit(
         d = dot2(kc[j].y, qv[h][1], d);
         d = dot2(kc[j].z, qv[h][2], d);
         d = dot2(kc[j].w, qv[h][3], d);
-        d = row_sum16(d);
-        sc[j][h] = (4 * j + row < valid) ? d * scale_log2 : -INFINITY;
+        sc[j][h] = row_sum16(d) * scale_log2;
       }
+    }
+    if (valid < P) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (4 * j + row >= valid) {
+#pragma unroll
+          for (int h = 0; h < G; ++h) sc[j][h] = -INFINITY;
+        }
     }
 
     float pr[4][G];
@@ -399,7 +403,7 @@ __device__ __forceinline__ void sweep_unit(
       for (int j = 0; j < 4; ++j) pr[j][h] = __builtin_amdgcn_exp2f(sc[j][h] - base);
       l[h] += (pr[0][h] + pr[1][h]) + (pr[2][h] + pr[3][h]);
     }
-    accumulate(vc, valid, [&](int j, int h) { return pr[j][h]; });
+    accumulate(vc, [&](int j, int h) { return pr[j][h]; });
   };
 
   // Rotation over NBUF register buffers: pages i+1 .. i+NBUF-1 stream in while page i is
@@ -407,7 +411,7 @@ __device__ __forceinline__ void sweep_unit(
   // block-table entry is requested only after the previous one has been consumed by issue().
   uint4 kbuf[NBUF][4], vbuf[NBUF][4];
 #pragma unroll
-  for (int t = 0; t < NBUF - 1; ++t) issue(kbuf[t], vbuf[t], entry(t), t < mine);
+  for (int t = 0; t < NBUF - 1; ++t) issue(kbuf[t], vbuf[t], entry(t), t);
   // The query loads (issued first) must have landed before the loop, so that the only loads in
   // flight inside it are the page buffers; the first pages stay in flight meanwhile
   // (s_waitcnt vmcnt(8 * (NBUF - 1)), expcnt 7, lgkmcnt 15).
@@ -418,7 +422,7 @@ __device__ __forceinline__ void sweep_unit(
 #pragma unroll
     for (int t = 0; t < NBUF; ++t) {
       const int ahead = i + t + NBUF - 1;
-      issue(kbuf[(t + NBUF - 1) % NBUF], vbuf[(t + NBUF - 1) % NBUF], ph_next, ahead < mine);
+      issue(kbuf[(t + NBUF - 1) % NBUF], vbuf[(t + NBUF - 1) % NBUF], ph_next, ahead);
       ph_next = entry(ahead + 1);
       if (i + t >= mine) goto swept;
       if constexpr (MF)
