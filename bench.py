@@ -348,7 +348,7 @@ def main():
                          "known-size reference that scales the FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
               "(position sharding across GPUs is a design note, not code).", file=sys.stderr)
         sys.exit(2)
 
