@@ -491,6 +491,15 @@ swept:
         L = fmaf(f, s_l[w][h], L);
         A = fmaf(f, s_acc[w][h][d], A);
       }
+    } else {
+      // No finite score: no position at all (every l is 0; an empty shard) or only NaN scores
+      // (a NaN query element; l is NaN), which must come out NaN like any NaN input.
+#pragma unroll
+      for (int w = 0; w < W; ++w) L += s_l[w][h];
+      A = L;
+    }
+    const bool nan_only = M == -INFINITY && __builtin_isnan(L);
+    if (M != -INFINITY || nan_only) {
       // Non-temporal: a thin stream of default-policy writes interleaved with the sweep's
       // reads costs far more HBM time than its bytes (measured ~4% of the sweep).
       if constexpr (MERGE)   // read by another workgroup of this launch (merge_if_last)
@@ -500,7 +509,7 @@ swept:
         __builtin_nontemporal_store(A / L, &out_o[(slot + h) * D + d]);
     }
     if (d == 0) {
-      float lse = (M == -INFINITY) ? -INFINITY : (M + log2f(L)) * kLn2;
+      float lse = nan_only ? NAN : (M == -INFINITY) ? -INFINITY : (M + log2f(L)) * kLn2;
       if (bad) lse = NAN;
       if constexpr (MERGE)
         __hip_atomic_store(&out_lse[slot + h], lse, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

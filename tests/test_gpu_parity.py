@@ -12,7 +12,8 @@ import pytest
 import torch
 
 import paper_2608_15473_amd as qf
-from parity import check, oracle_ref, run_gpu, say
+import oracle
+from parity import check, host_arrays, oracle_ref, run_gpu, say
 from workloads import WORKLOADS, make_case, workload_case
 
 pytestmark = pytest.mark.gpu
@@ -159,13 +160,53 @@ def test_repeat_calls_are_deterministic(gpu):
         assert np.array_equal(g1[key], g2[key], equal_nan=True), key
 
 
-def test_planted_large_logits_stay_finite(gpu):
+@pytest.mark.parametrize("hq", [16, 32], ids=["G2", "G4"])
+def test_planted_large_logits_stay_finite(gpu, hq):
     """Logits near 85 over many positions: ln Z ~ 91 > ln(FLT_MAX), where a naive fp32 sum of
-    exponentials overflows; every output must stay finite and match the oracle."""
-    case = make_case(1, 16, 8, [30000], [4], seed=160, planted=(400, 84.0, 86.0), device=gpu)
-    got, ref = _run(case, "planted ~85")
+    exponentials overflows; every output must stay finite and match the oracle (both score paths:
+    the VALU dot products at G = 2, the matrix cores at G = 4)."""
+    case = make_case(1, hq, 8, [30000], [4], seed=160, planted=(400, 84.0, 86.0), device=gpu)
+    got, ref = _run(case, f"planted ~85, {hq} query heads")
     assert np.all(np.isfinite(got["out"])) and np.all(np.isfinite(got["lse"]))
     assert np.all(ref["lse"] > 88.8)
+
+
+@pytest.mark.parametrize("G", [2, 4])
+def test_nan_inputs_reach_exactly_the_heads_that_read_them(gpu, G):
+    """A NaN is data, not masked (one reading of the paper's silence): a NaN query element poisons
+    that head only; a NaN key element poisons every head of its KV group (through the score); a
+    NaN value element poisons that dim of the group's outputs and leaves ln Z finite.  Every
+    other output stays bitwise as in the clean run, and the NaN pattern is the oracle's."""
+    ctx, S = [700, 300], [3, 2]
+    clean = make_case(2, 2 * G, 2, ctx, S, seed=330 + G, device=gpu)
+    base = run_gpu(clean)
+    bt = clean.block_table.long()
+    cases = {
+        "q": lambda c: c.q.__setitem__((0, 1, 17), float("nan")),
+        "k": lambda c: c.k_cache.__setitem__((int(bt[1, 5]), 1, 3, 40), float("nan")),
+        "v": lambda c: c.v_cache.__setitem__((int(bt[0, 20]), 0, 9, 77), float("nan")),
+    }
+    for what, poison in cases.items():
+        dirty = make_case(2, 2 * G, 2, ctx, S, seed=330 + G, device=gpu)
+        poison(dirty)
+        say(f"[parity] NaN in {what}, G={G}")
+        got = run_gpu(dirty)
+        a = host_arrays(dirty)
+        ro, rl = oracle.decode_unsplit(a["q"], a["k"], a["v"], a["bt"], a["ctx"], dirty.scale)
+        assert np.array_equal(np.isnan(got["out"]), np.isnan(ro)), what
+        assert np.array_equal(np.isnan(got["lse"]), np.isnan(rl)), what
+        hit = np.isnan(ro)
+        assert hit.any(), what
+        if what == "q":
+            assert hit[0, 1].all() and hit.sum() == 128
+        elif what == "k":
+            assert hit[1, G:2 * G].all() and hit.sum() == 128 * G
+        else:
+            assert hit[0, :G, 77].all() and hit.sum() == G and np.isfinite(got["lse"]).all()
+        keep = ~hit
+        assert np.array_equal(got["out_bits"][keep], base["out_bits"][keep]), what
+        keep_l = ~np.isnan(rl)
+        assert np.array_equal(got["lse"][keep_l], base["lse"][keep_l]), what
 
 
 def test_planted_secondary_reading(gpu):
