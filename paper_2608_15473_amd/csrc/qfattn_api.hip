@@ -145,7 +145,10 @@ int prepare_split(const qf_decode_desc* desc, const void* q, const void* k_cache
   // Short shards: short workgroups, prologue latency decides (keep a request on one XCD).
   const int64_t shard_pages = (d.max_pages_per_seq + d.max_shards - 1) / d.max_shards / chunks;
   p.order = shard_pages >= qf::kLongShardPages ? qf::kOrderByShardDesc : qf::kOrderByRequest;
-  p.deep = p.order == qf::kOrderByRequest && shard_pages >= qf::kDeepMinPages;
+  // Deep buffers cost occupancy (two wavefronts per SIMD instead of three), so a chunked sweep,
+  // whose chunk count fills exactly the resident workgroups of the two-buffer kernel, keeps two
+  // buffers (deep ones would leave a second, partial round: -2% on the 131,072-position share).
+  p.deep = p.order == qf::kOrderByRequest && shard_pages >= qf::kDeepMinPages && chunks == 1;
   p.scale_log2 = (float)((double)d.softmax_scale * 1.4426950408889634);
 
   sp->group = d.n_q_heads / d.n_kv_heads;

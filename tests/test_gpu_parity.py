@@ -294,6 +294,7 @@ _SAMPLES = {
     "qwen3-4b_b16_n36480_s32_l36": [(0, 0), (5, 13), (15, 31)],
     "qwen3-0.6b_b1_n1m_s16_l28_planted": [(0, 0), (0, 9)],
     "qwen3-4b_ragged_b64": "ragged",
+    "qwen3-0.6b_b1_n131072_s2_l28_planted": [(0, 2), (0, 15)],
 }
 
 
@@ -308,7 +309,7 @@ def test_full_size_workload_layer(gpu, name):
         order = np.argsort(n)
         pairs = [(int(order[0]), 3), (int(order[32]), 17), (int(order[-1]), 30)]
     got, ref = _run(case, f"{name} layer {layer}", pairs)
-    if name.endswith("planted"):
+    if WORKLOADS[name].planted:
         assert np.all(np.isfinite(got["out"])) and np.all(np.isfinite(got["lse"]))
         assert np.all(got["lse"] > 88.0)
     del case
@@ -317,7 +318,8 @@ def test_full_size_workload_layer(gpu, name):
 
 @pytest.mark.slow
 @pytest.mark.parametrize("name", ["qwen3-0.6b_b32_n32768_s64_l28", "qwen3-4b_b16_n36480_s32_l36",
-                                  "qwen3-0.6b_b1_n1m_s16_l28_planted"])
+                                  "qwen3-0.6b_b1_n1m_s16_l28_planted",
+                                  "qwen3-0.6b_b1_n131072_s2_l28_planted"])
 def test_full_size_every_layer_sampled(gpu, name):
     """Every layer of the multi-layer workloads, at its real shape: one (request, head) per layer,
     rotating through the batch and the heads."""

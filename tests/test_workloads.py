@@ -91,3 +91,15 @@ def test_planted_keys_reach_their_targets():
         for h in (2 * g, 2 * g + 1):
             s = case.scale * (K @ q[b, h])
             assert np.max(np.abs(s - t)) < 0.5     # bf16 rounding of the key moves it a little
+
+
+def test_one_gpu_share_of_the_long_request():
+    """The per-GPU share of the 2^20-position request sharded by position over 8 GPUs: an eighth
+    of its positions and of its planted keys, at the same model shape, two shards."""
+    whole = WORKLOADS["qwen3-0.6b_b1_n1m_s16_l28_planted"]
+    share = WORKLOADS["qwen3-0.6b_b1_n131072_s2_l28_planted"]
+    assert share.ctx * 8 == whole.ctx and share.shards == 2
+    assert (share.batch, share.n_q_heads, share.n_kv_heads, share.layers) == \
+        (whole.batch, whole.n_q_heads, whole.n_kv_heads, whole.layers)
+    assert share.planted and share.planted_count * 8 == whole.planted_count
+    assert share.max_pages() * 8 == whole.max_pages()

@@ -45,6 +45,7 @@ class Workload:
     shards: int | None         # uniform shard count, or None for ceil(n / ragged_shard_len)
     table: str                 # "identity" | "perm"
     planted: bool = False
+    planted_count: int = 400   # planted keys per (request, KV head)
     ragged_shard_len: int = 4096
     description: str = ""
 
@@ -94,6 +95,11 @@ WORKLOADS = {
         Workload("qwen3-4b_ragged_b64", 5, 64, 32, 8, 1, None, None, "perm",
                  description="1 layer, 64 requests, contexts log-uniform in [512, 131072], "
                              "ceil(n/4096) shards each"),
+        Workload("qwen3-0.6b_b1_n131072_s2_l28_planted", 6, 1, 16, 8, 28, 1 << 17, 2, "perm",
+                 planted=True, planted_count=50,
+                 description="one GPU's share of the 2^20-position request sharded by position "
+                             "over 8 GPUs: 28 layers, 131,072 positions, 2 shards, 50 planted "
+                             "keys per KV head (the 400 of the whole request, spread evenly)"),
     ]
 }
 
@@ -207,7 +213,7 @@ def workload_case(name: str, layer: int = 0, device="cpu", **override) -> Case:
     kw = dict(seed=1000 * w.index + layer, table=w.table, max_shards=w.max_shards(),
               max_pages=w.max_pages(), device=device)
     if w.planted:
-        kw["planted"] = (400, 84.0, 86.0)
+        kw["planted"] = (w.planted_count, 84.0, 86.0)
     kw.update(override)
     return make_case(w.batch, w.n_q_heads, w.n_kv_heads, lengths, w.shard_counts(lengths), **kw)
 
