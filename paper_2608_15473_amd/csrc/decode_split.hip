@@ -14,10 +14,10 @@
 // 8c..8c+7 of position 4j + r.  Each row is an independent online-softmax sweeper over the
 // positions r, r+4, r+8, r+12 of every page; rows and wavefronts merge once, at the end.
 //
-// Per page and lane, scores: at G = 4 query heads per KV head, on the matrix cores (the K tile
-// passes through LDS into the operand layout of four v_mfma_f32_16x16x32_bf16, which leave each
-// lane the scores of exactly the positions whose V it holds, for one head; the other heads' come
-// from the quad by DPP); otherwise with v_dot2c_f32_bf16 on the packed bf16 pairs and a 16-lane
+// Per page and lane, scores: at G = 4 or 8 query heads per KV head, on the matrix cores (the K
+// tile passes through LDS into the operand layout of four v_mfma_f32_16x16x32_bf16, which leave
+// each lane the scores of exactly the positions whose V it holds, for one head; the other heads'
+// come from neighbouring lanes by DPP); otherwise with v_dot2c_f32_bf16 on the packed bf16 pairs and a 16-lane
 // DPP all-reduce per score.  Both take exact bf16 products and fp32 sums.  Then exp2 in the log2
 // domain and fp32 FMAs for PV with the bf16 values unpacked by shift/mask.  The running max is
 // raised lazily (only when a score exceeds it by more than kLazy), so the O rescale is rare after
@@ -65,6 +65,23 @@ __device__ __forceinline__ float quad_bcast(float x, int h) {
     case 1: return __int_as_float(__builtin_amdgcn_mov_dpp(v, 0x55, 0xF, 0xF, true));
     case 2: return __int_as_float(__builtin_amdgcn_mov_dpp(v, 0xAA, 0xF, 0xF, true));
     default: return __int_as_float(__builtin_amdgcn_mov_dpp(v, 0xFF, 0xF, 0xF, true));
+  }
+}
+
+// Lane 8*(c/8) + h's value in every lane c of its 8-lane group (G = 8), or the quad's (G <= 4),
+// for the matrix path, where lane c holds the values of head c % G.  For G = 8 the quad broadcast
+// gives one half of each 8-lane group the right head, and a 4-lane row shift written only into
+// the other half's DPP banks (quads) completes it.
+template <int G>
+__device__ __forceinline__ float group_bcast(float x, int h) {
+  if constexpr (G == 1) {
+    return x;
+  } else if constexpr (G <= 4) {
+    return quad_bcast(x, h);
+  } else {
+    const float t = quad_bcast(x, h & 3);
+    return h < 4 ? __builtin_amdgcn_update_dpp(t, t, 0x114, 0xF, 0xA, false)   // row_shr:4 -> quads 1, 3
+                 : __builtin_amdgcn_update_dpp(t, t, 0x104, 0xF, 0x5, false);  // row_shl:4 -> quads 0, 2
   }
 }
 
@@ -210,11 +227,12 @@ __device__ __forceinline__ void sweep_unit(
   const int row = lane >> 4;
   const int col = lane & 15;
 
-  // With 4 heads per KV head the scores come from the matrix cores (process_mf below); otherwise
-  // the VALU computes them (process_valu).  Measured: the matrix path is 1-5% faster at G = 4,
-  // where the VALU path spends most of its issue slots on the dot products and reductions, and
-  // 1-2.5% slower at G = 2, where the VALU has slack and the LDS round trip only adds latency.
-  constexpr bool MF = G == 4;
+  // With 4 or 8 heads per KV head the scores come from the matrix cores (process_mf below);
+  // otherwise the VALU computes them (process_valu).  Measured: the matrix path is 1-5% faster at
+  // G = 4 and 27-32% faster at G = 8, where the VALU path spends most of its issue slots on the
+  // dot products and reductions, and 1-2.5% slower at G = 2, where the VALU has slack and the LDS
+  // round trip only adds latency.
+  constexpr bool MF = G >= 4;
 
   // Queries of the group.  VALU path: dims 8col..8col+7 of every head as packed bf16 pairs.
   // Matrix path: the queries are the 16 columns of the B operand of S^T = K Q^T (column c holds
@@ -236,7 +254,7 @@ __device__ __forceinline__ void sweep_unit(
 
   // Online-softmax state.  VALU path: every lane keeps (m, l) of all G heads for its row.  Matrix
   // path: lane (row, col) keeps them for head col % G only (m1, l1); the other heads' values sit
-  // in the same quad and are broadcast when needed.  acc: dims 8col..8col+7 of every head.
+  // in the same quad (8-lane group at G = 8) and are broadcast when needed.  acc: dims 8col..8col+7 of every head.
   float m[G], l[G], acc[G][8];
   float m1 = -INFINITY, l1 = 0.0f;
 #pragma unroll
@@ -349,7 +367,7 @@ __device__ __forceinline__ void sweep_unit(
     if (__builtin_amdgcn_ballot_w64(raise)) {   // rare after a shard's first page
 #pragma unroll
       for (int h = 0; h < G; ++h) {
-        const float a = G == 1 ? alpha : quad_bcast(alpha, h);
+        const float a = group_bcast<G>(alpha, h);
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[h][e] *= a;
       }
@@ -359,7 +377,7 @@ __device__ __forceinline__ void sweep_unit(
 #pragma unroll
     for (int i = 0; i < 4; ++i) pr[i] = __builtin_amdgcn_exp2f(sc[i] - base);
     l1 += (pr[0] + pr[1]) + (pr[2] + pr[3]);
-    accumulate(vc, [&](int j, int h) { return G == 1 ? pr[j] : quad_bcast(pr[j], h); });
+    accumulate(vc, [&](int j, int h) { return group_bcast<G>(pr[j], h); });
   };
 
   auto process_valu = [&](uint4* kc, uint4* vc, int pg) {
@@ -435,8 +453,8 @@ swept:
   if constexpr (MF) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      m[h] = G == 1 ? m1 : quad_bcast(m1, h);
-      l[h] = G == 1 ? l1 : quad_bcast(l1, h);
+      m[h] = group_bcast<G>(m1, h);
+      l[h] = group_bcast<G>(l1, h);
     }
   }
 

@@ -115,7 +115,7 @@ def test_physical_page_placement_is_bitwise_irrelevant(gpu):
         assert np.array_equal(ga[key], gb[key], equal_nan=True), key
 
 
-@pytest.mark.parametrize("G", [2, 4])
+@pytest.mark.parametrize("G", [2, 4, 8])
 def test_garbage_past_the_last_position_is_never_used(gpu, G):
     """The slots of a request's last page past its last position hold no position: NaN and Inf
     there (in K and in V) must leave every result bitwise as it is with finite values there, in
@@ -160,18 +160,18 @@ def test_repeat_calls_are_deterministic(gpu):
         assert np.array_equal(g1[key], g2[key], equal_nan=True), key
 
 
-@pytest.mark.parametrize("hq", [16, 32], ids=["G2", "G4"])
+@pytest.mark.parametrize("hq", [16, 32, 64], ids=["G2", "G4", "G8"])
 def test_planted_large_logits_stay_finite(gpu, hq):
     """Logits near 85 over many positions: ln Z ~ 91 > ln(FLT_MAX), where a naive fp32 sum of
     exponentials overflows; every output must stay finite and match the oracle (both score paths:
-    the VALU dot products at G = 2, the matrix cores at G = 4)."""
+    the VALU dot products at G = 2, the matrix cores at G = 4 and 8)."""
     case = make_case(1, hq, 8, [30000], [4], seed=160, planted=(400, 84.0, 86.0), device=gpu)
     got, ref = _run(case, f"planted ~85, {hq} query heads")
     assert np.all(np.isfinite(got["out"])) and np.all(np.isfinite(got["lse"]))
     assert np.all(ref["lse"] > 88.8)
 
 
-@pytest.mark.parametrize("G", [2, 4])
+@pytest.mark.parametrize("G", [2, 4, 8])
 def test_nan_inputs_reach_exactly_the_heads_that_read_them(gpu, G):
     """A NaN is data, not masked (one reading of the paper's silence): a NaN query element poisons
     that head only; a NaN key element poisons every head of its KV group (through the score); a
