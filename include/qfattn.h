@@ -96,7 +96,8 @@ int qf_attn_decode_split_workspace_size(const qf_decode_desc* desc, size_t* byte
  *               Not written for empty shards or for slots s >= S_b (§5: never read).
  *   part_lse    fp32 [B, max_shards, Hq], 4-byte aligned: natural-log ln Z of shard s; -inf for
  *               an empty shard and for every slot s >= S_b; NaN if request b's inputs were out
- *               of range (see above).
+ *               of range (see above), and NaN (O too) where a NaN in q, K or V reaches the
+ *               shard's scores (a NaN in V alone poisons only that dim of O).
  *   workspace   device buffer of at least qf_attn_decode_split_workspace_size() bytes, 16-byte
  *               aligned; may be NULL when that size is 0.  Its contents need no initialisation
  *               and are garbage afterwards.
