@@ -317,6 +317,20 @@ def test_full_size_workload_layer(gpu, name):
 
 
 @pytest.mark.slow
+@pytest.mark.parametrize("hq,hkv", [(64, 8), (32, 4)], ids=["G8_64q8kv", "G8_32q4kv"])
+def test_eight_heads_per_kv_head_long_requests_sampled(gpu, hq, hkv):
+    """Eight query heads per KV head (the matrix-core scores with 8-lane broadcasts) on long
+    requests (chunked shards, the long-shard dispatch), sampled heads of every KV group; the
+    short-shard dispatch at G = 8 is in the small cases above."""
+    for B, n, S in [(4, 32768, 8), (1, 300000, 2)]:
+        case = make_case(B, hq, hkv, [n] * B, S, seed=870 + hq + B, device=gpu)
+        pairs = [(b, (5 * b + 8 * g + b % 8) % hq) for b in range(B) for g in range(hkv)]
+        _run(case, f"G=8 {hq}q/{hkv}kv B={B} n={n} S={S}", pairs)
+        del case
+        torch.cuda.empty_cache()
+
+
+@pytest.mark.slow
 @pytest.mark.parametrize("name", ["qwen3-0.6b_b32_n32768_s64_l28", "qwen3-4b_b16_n36480_s32_l36",
                                   "qwen3-0.6b_b1_n1m_s16_l28_planted",
                                   "qwen3-0.6b_b1_n131072_s2_l28_planted"])
