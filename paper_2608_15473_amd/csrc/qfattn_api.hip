@@ -29,8 +29,12 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 // second round (measured on the 1M-token shape, 128 units: 6 chunks beat 16 and 12).  The count
 // depends on the descriptor and the device's occupancy for the kernel only, so a given shape on a
 // given GPU always runs the same decomposition (and gives the same bits); with no device to ask
-// (a host without a GPU sizing a workspace) it assumes an MI355X at three workgroups per CU.
-constexpr int64_t kFallbackResident = 768;
+// (a host without a GPU sizing a workspace) it assumes the counts this build reaches on an MI355X
+// (256 CUs; 4 workgroups per CU at G = 1, 3 at G = 2 and 4, 2 at G = 8), which a GPU test checks
+// against the device.
+int64_t fallback_resident(int group) {
+  return group == 1 ? 1024 : group == 8 ? 512 : 768;
+}
 constexpr int64_t kMinPagesPerWave = 2;
 
 int check_desc(const qf_decode_desc* d) {
@@ -60,8 +64,9 @@ int check_desc(const qf_decode_desc* d) {
 int64_t choose_chunks(const qf_decode_desc* d) {
   const int64_t units = (int64_t)d->batch * d->n_kv_heads * d->max_shards;
   if (units <= 0) return 1;
-  int64_t slots = qf::split_resident_workgroups(d->n_q_heads / d->n_kv_heads);
-  if (slots <= 0) slots = kFallbackResident;
+  const int group = d->n_q_heads / d->n_kv_heads;
+  int64_t slots = qf::split_resident_workgroups(group);
+  if (slots <= 0) slots = fallback_resident(group);
   if (units >= slots) return 1;
   const int64_t est_pages = (d->max_pages_per_seq + d->max_shards - 1) / d->max_shards;
   int64_t c = slots / units;
