@@ -388,12 +388,15 @@ def main():
     S = cases[0].max_shards
     ab = [algorithmic_bytes(c) for c in cases]
 
-    po = torch.empty((B, S, Hq, D), dtype=torch.float32, device=dev)
-    pl = torch.empty((B, S, Hq), dtype=torch.float32, device=dev)
+    desc = qf.make_desc(cases[0].q, cases[0].k_cache, cases[0].block_table, S, cases[0].scale)
+    # The two-launch step leaves a chunked shape's sub-shard chunks as slots of the partials (the
+    # combine merges them directly: no chunk fold launch), so it needs S * C slots, no workspace.
+    C = 1 if args.one_launch else qf.split_chunks(desc)
+    po = torch.empty((B, S * C, Hq, D), dtype=torch.float32, device=dev)
+    pl = torch.empty((B, S * C, Hq), dtype=torch.float32, device=dev)
     out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=dev)
     lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
-    desc = qf.make_desc(cases[0].q, cases[0].k_cache, cases[0].block_table, S, cases[0].scale)
-    need = qf.decode_workspace_size(desc) if args.one_launch else qf.workspace_size(desc)
+    need = qf.decode_workspace_size(desc) if args.one_launch else 0
     ws = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
     counters = torch.zeros(B * Hkv, dtype=torch.int32, device=dev)  # zero-filled once
 
@@ -403,7 +406,7 @@ def main():
     plans = [] if args.one_launch else [
         qf.DecodeStepPlan(c.q, c.k_cache, c.v_cache, c.block_table, c.ctx_lens, c.n_shards,
                           max_shards=S, scale=c.scale, part_out=po, part_lse=pl, out=out, lse=lse,
-                          workspace=ws) for c in cases]
+                          fold_chunks=False) for c in cases]
 
     def step(events=None):
         base = turn[0]
@@ -473,6 +476,7 @@ def main():
                    "head_dim": D, "page": 16, "layers": L, "max_shards": S,
                    "context": w.ctx if w.ctx else "ragged", "kv_dtype": "bf16",
                    "kv_bytes_per_step": kv_step, "workspace_bytes": need,
+                   "chunks_per_shard": C,
                    "resident_layer_copies": copies},
         "hbm_peak_frac": round(value / HBM_PEAK_GBS, 4),
         "attended_tokens_per_s_per_layer": round(attended / (ms_per_step / 1e3 / L), 1),

@@ -13,7 +13,7 @@
  * partition, any order; an empty shard is ln Z = -inf with a vector that is never read).
  *
  * Entry points: the sweep and its merge (qf_attn_decode_split, qf_attn_combine, or both in one
- * launch: qf_attn_decode); the decode step
+ * launch: qf_attn_decode; qf_attn_decode_split_unfolded leaves sub-shard chunks as extra slots); the decode step
  * around them (qf_attn_combine_current folds in the current token, qf_kv_append writes it to the
  * cache, qf_attn_combine_current_append does both in one launch); the dense products of a decoder block (qf_linear) and the sweep sharing one launch with
  * one of them (qf_attn_decode_split_beside); and a host-side simulation of the layer-wise decode
@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define QF_VERSION 3
+#define QF_VERSION 4
 
 #define QF_OK 0
 #define QF_EINVAL (-1)       /* null pointer, negative or inconsistent size, Hq % Hkv != 0   */
@@ -107,6 +107,36 @@ int qf_attn_decode_split(const qf_decode_desc* desc, const void* q, const void* 
                          const void* v_cache, const int32_t* block_table,
                          const int32_t* ctx_lens, const int32_t* n_shards, float* part_out,
                          float* part_lse, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Sub-shard chunks per shard that the sweep uses for this shape (host call): C >= 1; C > 1 exactly
+ * when qf_attn_decode_split_workspace_size() is nonzero (few (request, KV head, shard) units:
+ * the pages of every shard are cut into C consecutive ranges of ceil(len / C) pages, len the
+ * shard's page count, the last ranges shorter or empty, so that the sweep fills the GPU once).
+ * Like the workspace size it depends on the device's resident workgroups.  Returns QF_OK,
+ * QF_EINVAL or QF_EUNSUPPORTED.
+ */
+int qf_attn_decode_split_chunks(const qf_decode_desc* desc, int32_t* chunks);
+
+/*
+ * The sweep of qf_attn_decode_split without folding the sub-shard chunks into their shards: slot
+ * s * C + c of request b receives the pair (O, ln Z) of chunk c of shard s, C =
+ * qf_attn_decode_split_chunks() (with C == 1 the slots are the shards and this call is
+ * qf_attn_decode_split).  A chunk is itself a shard of a finer split of the same cache (§5: any
+ * partition), so qf_attn_combine over the max_shards * C slots gives the result of the folded
+ * sweep followed by the combine, up to the order of the fp32 sums, with one launch fewer and no
+ * workspace: for callers that need only the merged attention, not per-shard partials.
+ *
+ *   q ... n_shards   as for qf_attn_decode_split.
+ *   slot_out    fp32 [B, max_shards * C, Hq, D], 16-byte aligned: O of every non-empty chunk.
+ *   slot_lse    fp32 [B, max_shards * C, Hq], 4-byte aligned: ln Z of every chunk slot; -inf for
+ *               an empty chunk and for every chunk of a slot s >= S_b; NaN as for part_lse.
+ *   stream      hipStream_t.
+ */
+int qf_attn_decode_split_unfolded(const qf_decode_desc* desc, const void* q, const void* k_cache,
+                                  const void* v_cache, const int32_t* block_table,
+                                  const int32_t* ctx_lens, const int32_t* n_shards,
+                                  float* slot_out, float* slot_lse, void* stream);
 
 /*
  * The sweep and the merge in ONE launch: the result of qf_attn_decode_split followed by

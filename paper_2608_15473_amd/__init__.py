@@ -29,6 +29,8 @@ from .binding import (  # noqa: F401
     attn_decode,
     attn_decode_split,
     attn_decode_split_beside,
+    attn_decode_split_unfolded,
+    split_chunks,
     DecodeStepPlan,
     decode_workspace_size,
     kv_append,

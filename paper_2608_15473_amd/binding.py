@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(_HERE, "lib", "libqfattn.so")
 
 QF_OK, QF_EINVAL, QF_EUNSUPPORTED, QF_EALIGN, QF_EHIP = 0, -1, -2, -3, -4
 EXPORTED = ("qf_attn_decode_split_workspace_size", "qf_attn_decode_split", "qf_attn_combine",
+            "qf_attn_decode_split_chunks", "qf_attn_decode_split_unfolded",
             "qf_attn_decode_workspace_size", "qf_attn_decode",
             "qf_attn_combine_current", "qf_attn_combine_current_append", "qf_kv_append",
             "qf_linear", "qf_attn_decode_split_beside",
@@ -64,6 +65,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.qf_attn_decode_split.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp, vp, vp,
                                          vp, vp, sz, vp]
     lib.qf_attn_combine.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp]
+    lib.qf_attn_decode_split_chunks.argtypes = [ctypes.POINTER(DecodeDesc),
+                                                ctypes.POINTER(ctypes.c_int32)]
+    lib.qf_attn_decode_split_unfolded.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp,
+                                                  vp, vp, vp, vp]
     lib.qf_attn_decode_workspace_size.argtypes = [ctypes.POINTER(DecodeDesc), ctypes.POINTER(sz)]
     lib.qf_attn_decode.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                    sz, vp, ctypes.c_int64, vp]
@@ -83,6 +88,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.qf_last_error.argtypes = []
     lib.qf_version.argtypes = []
     for name in ("qf_attn_decode_split_workspace_size", "qf_attn_decode_split",
+                 "qf_attn_decode_split_chunks", "qf_attn_decode_split_unfolded",
                  "qf_attn_decode_workspace_size", "qf_attn_decode",
                  "qf_attn_combine", "qf_attn_combine_current", "qf_attn_combine_current_append",
                  "qf_kv_append",
@@ -130,10 +136,19 @@ def workspace_size(desc: DecodeDesc) -> int:
     return n.value
 
 
+def split_chunks(desc: DecodeDesc) -> int:
+    """Sub-shard chunks per shard the sweep uses for this shape (qf_attn_decode_split_chunks)."""
+    c = ctypes.c_int32(0)
+    _check(load_library().qf_attn_decode_split_chunks(ctypes.byref(desc), ctypes.byref(c)))
+    return c.value
+
+
 def _split_call(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards, scale,
-                part_out, part_lse, workspace, max_pages):
-    """Checks and allocations of qf_attn_decode_split: returns (C arguments, descriptor, part_out,
-    part_lse, workspace, n_shards), the last three as tensors the C arguments point into."""
+                part_out, part_lse, workspace, max_pages, unfolded=False):
+    """Checks and allocations of qf_attn_decode_split (or, ``unfolded``, of
+    qf_attn_decode_split_unfolded, whose slot arrays hold max_shards * chunks slots and which takes
+    no workspace): returns (C arguments, descriptor, part_out, part_lse, workspace, n_shards), the
+    last three as tensors the C arguments point into."""
     _require(q, "q", torch.bfloat16, 3)
     _require(k_cache, "k_cache", torch.bfloat16, 4)
     _require(v_cache, "v_cache", torch.bfloat16, 4)
@@ -154,19 +169,26 @@ def _split_call(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards
         scale = q.shape[-1] ** -0.5
     desc = make_desc(q, k_cache, block_table, max_shards, scale, max_pages=max_pages)
     Hq, D = q.shape[1], q.shape[2]
+    slots = max_shards * (split_chunks(desc) if unfolded else 1)
     if part_out is None:
-        part_out = torch.empty((B, max_shards, Hq, D), dtype=torch.float32, device=q.device)
+        part_out = torch.empty((B, slots, Hq, D), dtype=torch.float32, device=q.device)
     if part_lse is None:
-        part_lse = torch.empty((B, max_shards, Hq), dtype=torch.float32, device=q.device)
+        part_lse = torch.empty((B, slots, Hq), dtype=torch.float32, device=q.device)
     _require(part_out, "part_out", torch.float32)
     _require(part_lse, "part_lse", torch.float32)
+    if tuple(part_out.shape) != (B, slots, Hq, D) or tuple(part_lse.shape) != (B, slots, Hq):
+        raise QFError(QF_EINVAL, f"partial outputs must be [{B}, {slots}, {Hq}, {D}] and "
+                                 f"[{B}, {slots}, {Hq}] (got {tuple(part_out.shape)} and "
+                                 f"{tuple(part_lse.shape)})")
+    head = (ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+            _ptr(ctx_lens), _ptr(n_shards), _ptr(part_out), _ptr(part_lse))
+    if unfolded:
+        return head, desc, part_out, part_lse, None, n_shards
     need = workspace_size(desc)
     if need and workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    args = (ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
-            _ptr(ctx_lens), _ptr(n_shards), _ptr(part_out), _ptr(part_lse), _ptr(workspace),
-            ws_bytes)
+    args = head + (_ptr(workspace), ws_bytes)
     return args, desc, part_out, part_lse, workspace, n_shards
 
 
@@ -185,6 +207,24 @@ def attn_decode_split(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_
     stream = torch.cuda.current_stream(q.device).cuda_stream
     _check(load_library().qf_attn_decode_split(*args, ctypes.c_void_p(stream)))
     return part_out, part_lse
+
+
+def attn_decode_split_unfolded(q, k_cache, v_cache, block_table, ctx_lens, n_shards,
+                               max_shards=None, scale=None, slot_out=None, slot_lse=None,
+                               max_pages=None):
+    """The sweep with its sub-shard chunks left as slots (qf_attn_decode_split_unfolded).
+
+    Arguments as for ``attn_decode_split``.  Returns (slot_out fp32 [B, S_max * C, Hq, D],
+    slot_lse fp32 [B, S_max * C, Hq]), C = the sweep's chunks per shard: slot s * C + c is chunk c
+    of shard s.  ``attn_combine`` over them gives the merged attention with one launch fewer than
+    ``attn_decode_split`` when C > 1.
+    """
+    args, desc, slot_out, slot_lse, _, n_shards = _split_call(
+        q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards, scale, slot_out,
+        slot_lse, None, max_pages, unfolded=True)
+    stream = torch.cuda.current_stream(q.device).cuda_stream
+    _check(load_library().qf_attn_decode_split_unfolded(*args, ctypes.c_void_p(stream)))
+    return slot_out, slot_lse
 
 
 def attn_decode_split_beside(q, k_cache, v_cache, block_table, ctx_lens, n_shards, beside,
@@ -228,6 +268,9 @@ class DecodeStepPlan:
 
     The arguments are those of ``attn_decode_split`` (plus ``out`` / ``lse`` of ``attn_combine``);
     every tensor, the workspace included, is allocated here when not given and kept by the plan.
+    With ``fold_chunks=False`` the sweep is ``attn_decode_split_unfolded`` (its sub-shard chunks
+    stay slots of part_out / part_lse, [B, S_max * C, ...], and the combine merges them: one launch
+    fewer when the shape is chunked); otherwise part_out / part_lse are the per-shard partials.
     Calling the plan enqueues the two library calls on ``stream`` (default: the current stream at
     construction) with the pointers taken at construction, so the caller updates tensors in
     place (e.g. the query, the cache, ctx_lens) and never reallocates them; per call the host does
@@ -237,10 +280,10 @@ class DecodeStepPlan:
 
     def __init__(self, q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards=None,
                  scale=None, part_out=None, part_lse=None, out=None, lse=None, workspace=None,
-                 max_pages=None, stream=None):
+                 max_pages=None, stream=None, fold_chunks=True):
         args, desc, part_out, part_lse, workspace, n_shards = _split_call(
             q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards, scale, part_out,
-            part_lse, workspace, max_pages)
+            part_lse, workspace, max_pages, unfolded=not fold_chunks)
         B, S, Hq, D = part_out.shape
         if out is None:
             out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=q.device)
@@ -257,7 +300,7 @@ class DecodeStepPlan:
                       out, lse, workspace, desc)
         self._desc = desc
         lib = load_library()
-        self._split = lib.qf_attn_decode_split
+        self._split = lib.qf_attn_decode_split if fold_chunks else lib.qf_attn_decode_split_unfolded
         self._combine = lib.qf_attn_combine
         self._split_args = args + (ctypes.c_void_p(stream),)
         self._combine_args = (B, Hq, D, S, _ptr(part_out), _ptr(part_lse), _ptr(out), _ptr(lse),
@@ -265,7 +308,7 @@ class DecodeStepPlan:
         self.part_out, self.part_lse, self.out, self.lse = part_out, part_lse, out, lse
 
     def split(self):
-        """Enqueue the sweep (qf_attn_decode_split) into part_out / part_lse."""
+        """Enqueue the sweep (qf_attn_decode_split, or its unfolded form) into part_out / part_lse."""
         rc = self._split(*self._split_args)
         if rc != QF_OK:
             raise QFError(rc, load_library().qf_last_error().decode())

@@ -83,6 +83,7 @@ size_t workspace_bytes(const qf_decode_desc* d, int64_t chunks) {
 // Everything qf_attn_decode_split checks and derives before launching.
 struct Split {
   bool noop = false;
+  bool fold = true;  // chunks folded into their shards (qf_attn_decode_split) or left as slots
   int group = 1;
   int64_t chunks = 1;
   qf::SplitParams p{};
@@ -92,7 +93,7 @@ struct Split {
 int prepare_split(const qf_decode_desc* desc, const void* q, const void* k_cache,
                   const void* v_cache, const int32_t* block_table, const int32_t* ctx_lens,
                   const int32_t* n_shards, float* part_out, float* part_lse, void* workspace,
-                  size_t workspace_size, Split* sp) {
+                  size_t workspace_size, Split* sp, bool fold = true) {
   int rc = check_desc(desc);
   if (rc) return rc;
   const qf_decode_desc& d = *desc;
@@ -112,7 +113,7 @@ int prepare_split(const qf_decode_desc* desc, const void* q, const void* k_cache
                 (long long)d.batch * d.max_pages_per_seq, d.num_pages);
 
   const int64_t chunks = choose_chunks(&d);
-  const size_t need = workspace_bytes(&d, chunks);
+  const size_t need = fold ? workspace_bytes(&d, chunks) : 0;
   if (need) {
     if (!workspace) return fail(QF_EINVAL, "this shape needs %zu bytes of workspace", need);
     if (workspace_size < need)
@@ -130,7 +131,7 @@ int prepare_split(const qf_decode_desc* desc, const void* q, const void* k_cache
   p.ctx_lens = ctx_lens;
   p.n_shards = n_shards;
   const size_t states = (size_t)d.batch * d.max_shards * chunks * d.n_q_heads;
-  if (chunks > 1) {
+  if (chunks > 1 && fold) {
     p.out_o = static_cast<float*>(workspace);
     p.out_lse = static_cast<float*>(workspace) + states * qf::kHeadDim;
   } else {
@@ -158,8 +159,9 @@ int prepare_split(const qf_decode_desc* desc, const void* q, const void* k_cache
 
   sp->group = d.n_q_heads / d.n_kv_heads;
   sp->chunks = chunks;
+  sp->fold = fold;
   sp->p = p;
-  if (chunks > 1) {
+  if (chunks > 1 && fold) {
     qf::MergeParams& m = sp->chunk_merge;
     m.in_o = p.out_o;
     m.in_lse = p.out_lse;
@@ -180,7 +182,7 @@ size_t fused_workspace_bytes(const qf_decode_desc* d, int64_t chunks) {
 
 // After the sweep's launch: fold the chunks of each shard into the caller's per-shard partials.
 int finish_split(const Split& sp, hipStream_t s) {
-  if (sp.chunks <= 1) return QF_OK;
+  if (sp.chunks <= 1 || !sp.fold) return QF_OK;
   const hipError_t e = qf::launch_merge(sp.chunk_merge, false, s);
   if (e != hipSuccess) return fail(QF_EHIP, "chunk merge launch: %s", hipGetErrorString(e));
   return QF_OK;
@@ -269,6 +271,32 @@ int qf_attn_decode_split(const qf_decode_desc* desc, const void* q, const void* 
   const hipError_t e = qf::launch_decode_split(sp.p, sp.group, s);
   if (e != hipSuccess) return fail(QF_EHIP, "decode_split launch: %s", hipGetErrorString(e));
   return finish_split(sp, s);
+}
+
+int qf_attn_decode_split_chunks(const qf_decode_desc* desc, int32_t* chunks) {
+  g_error[0] = 0;
+  const int rc = check_desc(desc);
+  if (rc) return rc;
+  if (!chunks) return fail(QF_EINVAL, "chunks is NULL");
+  *chunks = (int32_t)choose_chunks(desc);
+  return QF_OK;
+}
+
+int qf_attn_decode_split_unfolded(const qf_decode_desc* desc, const void* q, const void* k_cache,
+                                  const void* v_cache, const int32_t* block_table,
+                                  const int32_t* ctx_lens, const int32_t* n_shards,
+                                  float* slot_out, float* slot_lse, void* stream) {
+  g_error[0] = 0;
+  Split sp;
+  const int rc = prepare_split(desc, q, k_cache, v_cache, block_table, ctx_lens, n_shards,
+                               slot_out, slot_lse, nullptr, 0, &sp, false);
+  if (rc || sp.noop) return rc;
+  if ((int64_t)desc->max_shards * sp.chunks > (int64_t)INT32_MAX)
+    return fail(QF_EINVAL, "max_shards * chunks exceeds int32");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const hipError_t e = qf::launch_decode_split(sp.p, sp.group, s);
+  if (e != hipSuccess) return fail(QF_EHIP, "decode_split launch: %s", hipGetErrorString(e));
+  return QF_OK;
 }
 
 int qf_attn_decode_workspace_size(const qf_decode_desc* desc, size_t* bytes) {

@@ -301,3 +301,39 @@ def test_binding_refuses_cpu_tensors():
     k = torch.zeros(4, 8, 16, 128, dtype=torch.bfloat16)
     with pytest.raises(qf.QFError):
         qf.attn_decode_split(q, k, k, None, torch.zeros(1, dtype=torch.int32), 1)
+
+
+def test_chunk_count_agrees_with_the_workspace():
+    """qf_attn_decode_split_chunks gives the chunk count behind the workspace size: C > 1 exactly
+    when a workspace is needed, whose size is then B * S * C * Hq * (128 + 1) fp32."""
+    lib = load_library()
+    for kw in [dict(batch=1, max_shards=16, max_pages_per_seq=65536, num_pages=65536),
+               dict(batch=1, max_shards=8, max_pages_per_seq=288, num_pages=288),
+               dict(batch=3, max_shards=32, max_pages_per_seq=65536, num_pages=65536),
+               dict(batch=1, n_q_heads=8, n_kv_heads=1, max_shards=1, max_pages_per_seq=65536,
+                    num_pages=65536),
+               dict(batch=2, max_shards=4)]:
+        d = _desc(**kw)
+        c = ctypes.c_int32(0)
+        assert lib.qf_attn_decode_split_chunks(ctypes.byref(d), ctypes.byref(c)) == qf.QF_OK
+        rc, n = _ws(d)
+        assert rc == 0 and c.value >= 1
+        per_chunk = d.batch * d.max_shards * d.n_q_heads * (128 + 1) * 4
+        assert n == (0 if c.value == 1 else c.value * per_chunk), (kw, c.value, n)
+    bad = _desc(n_q_heads=12, n_kv_heads=8)
+    assert lib.qf_attn_decode_split_chunks(ctypes.byref(bad), ctypes.byref(c)) == qf.QF_EINVAL
+    assert lib.qf_attn_decode_split_chunks(ctypes.byref(_desc()), None) == qf.QF_EINVAL
+
+
+def test_unfolded_sweep_rejects_before_launch():
+    """qf_attn_decode_split_unfolded validates the descriptor and its pointers on the host."""
+    lib = load_library()
+    a = ctypes.c_void_p(4096)
+    fn = lib.qf_attn_decode_split_unfolded
+    d = _desc()
+    assert fn(ctypes.byref(d), a, a, a, None, a, a, a, None, None) == qf.QF_EINVAL
+    assert fn(ctypes.byref(d), ctypes.c_void_p(4098), a, a, None, a, a, a, a, None) == qf.QF_EALIGN
+    bad = _desc(head_dim=64)
+    assert fn(ctypes.byref(bad), a, a, a, None, a, a, a, a, None) == qf.QF_EUNSUPPORTED
+    empty = _desc(batch=0)
+    assert fn(ctypes.byref(empty), None, None, None, None, None, None, None, None, None) == qf.QF_OK

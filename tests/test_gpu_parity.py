@@ -380,6 +380,68 @@ def _one_launch_vs_two(case, workspace=None, counters=None):
     return out1, lse1
 
 
+_UNFOLDED = {  # (batch, Hq, Hkv, ctx_lens, n_shards)
+    "unchunked": (3, 16, 8, [1000, 37, 517], [5, 2, 3]),
+    "chunked one request": (1, 16, 8, [4607], 8),
+    "chunked long units": (2, 16, 8, [70001, 9], [1, 1]),
+    "chunked G4": (1, 32, 8, [50000], 2),
+    "chunked G8": (1, 64, 8, [40000], 2),
+    "chunked empty shards": (3, 16, 8, [0, 16, 30000], [3, 4, 5]),
+}
+
+
+@pytest.mark.parametrize("name", list(_UNFOLDED))
+def test_unfolded_sweep_then_combine(gpu, name):
+    """The sweep with its sub-shard chunks left as slots (qf_attn_decode_split_unfolded), merged
+    by one combine over S * C slots: the oracle's gates, and close to the folded sweep plus
+    combine (bitwise when there are no chunks; otherwise the fp32 sums are grouped differently:
+    lse within 8 fp32 ulp, out within one bf16 step or 1e-5 of its row's largest magnitude, since
+    an element far below that can move by several of its own bf16 steps); empty chunks and the
+    chunks of unused shard slots carry -inf; a plan with fold_chunks=False equals it."""
+    B, hq, hkv, ctx, S = _UNFOLDED[name]
+    case = make_case(B, hq, hkv, ctx, S, seed=880 + len(name), device=gpu)
+    args = (case.q, case.k_cache, case.v_cache, case.block_table, case.ctx_lens, case.n_shards)
+    C = qf.split_chunks(qf.make_desc(case.q, case.k_cache, case.block_table, case.max_shards,
+                                     case.scale))
+    assert (C > 1) == (name != "unchunked")
+    so = torch.full((B, case.max_shards * C, hq, 128), float("nan"), device=gpu)
+    sl = torch.full((B, case.max_shards * C, hq), float("nan"), device=gpu)
+    qf.attn_decode_split_unfolded(*args, max_shards=case.max_shards, scale=case.scale,
+                                  slot_out=so, slot_lse=sl)
+    out_u, lse_u = qf.attn_combine(so, sl)
+    plan = qf.DecodeStepPlan(*args, max_shards=case.max_shards, scale=case.scale,
+                             fold_chunks=False)
+    out_p, lse_p = plan()
+    folded = run_gpu(case)
+    torch.cuda.synchronize()
+    say(f"[parity] unfolded sweep: {name}, {C} chunks per shard")
+    assert torch.equal(_bits(out_p), _bits(out_u)) and torch.equal(_bits(lse_p), _bits(lse_u))
+    lse_f = torch.from_numpy(folded["lse"]).to(gpu)
+    bits_f = torch.from_numpy(folded["out_bits"]).to(gpu)
+    if C == 1:
+        assert torch.equal(_bits(lse_u), _bits(lse_f)) and torch.equal(_bits(out_u), bits_f)
+    else:
+        a, b = lse_u.double(), lse_f.double()
+        same = (a == b) | (torch.isnan(a) & torch.isnan(b))
+        assert (same | ((a - b).abs() <= 8 * 2.0 ** -23 * b.abs())).all()
+        fo, uo = bits_f.view(torch.bfloat16).float(), out_u.float()
+        row = fo.abs().amax(dim=-1, keepdim=True)
+        assert ((uo - fo).abs() <= torch.maximum(fo.abs() * 2.0 ** -7, row * 1e-5)).all()
+    # every slot written: -inf where a chunk or a shard slot holds no position
+    lse_slots = sl.cpu().numpy()
+    assert not np.isnan(lse_slots).any()
+    n_sh = case.n_shards.cpu().numpy()
+    for b in range(B):
+        assert np.all(lse_slots[b, n_sh[b] * C:] == -np.inf)
+        if int(case.ctx_lens[b]) == 0:
+            assert np.all(lse_slots[b] == -np.inf)
+    ref = oracle_ref(case)
+    got = dict(folded)
+    got["out"], got["lse"] = out_u.float().cpu().numpy(), lse_u.cpu().numpy()
+    got["out_bits"] = _bits(out_u).cpu().numpy()
+    check(case, got, ref, label=f"unfolded {name}")
+
+
 _ONE_LAUNCH = {
     "G1": dict(batch=3, n_q_heads=2, n_kv_heads=2, ctx_lens=[1000, 37, 517], n_shards=[5, 2, 3]),
     "G2": dict(batch=3, n_q_heads=4, n_kv_heads=2, ctx_lens=[1000, 37, 517], n_shards=[5, 2, 3]),
