@@ -295,6 +295,7 @@ _SAMPLES = {
     "qwen3-0.6b_b1_n1m_s16_l28_planted": [(0, 0), (0, 9)],
     "qwen3-4b_ragged_b64": "ragged",
     "qwen3-0.6b_b1_n131072_s2_l28_planted": [(0, 2), (0, 15)],
+    "qwen3-32b_b16_n32768_s32_l64": [(0, 0), (6, 29), (15, 63)],
 }
 
 
@@ -333,7 +334,8 @@ def test_eight_heads_per_kv_head_long_requests_sampled(gpu, hq, hkv):
 @pytest.mark.slow
 @pytest.mark.parametrize("name", ["qwen3-0.6b_b32_n32768_s64_l28", "qwen3-4b_b16_n36480_s32_l36",
                                   "qwen3-0.6b_b1_n1m_s16_l28_planted",
-                                  "qwen3-0.6b_b1_n131072_s2_l28_planted"])
+                                  "qwen3-0.6b_b1_n131072_s2_l28_planted",
+                                  "qwen3-32b_b16_n32768_s32_l64"])
 def test_full_size_every_layer_sampled(gpu, name):
     """Every layer of the multi-layer workloads, at its real shape: one (request, head) per layer,
     rotating through the batch and the heads."""

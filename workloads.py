@@ -95,6 +95,9 @@ WORKLOADS = {
         Workload("qwen3-4b_ragged_b64", 5, 64, 32, 8, 1, None, None, "perm",
                  description="1 layer, 64 requests, contexts log-uniform in [512, 131072], "
                              "ceil(n/4096) shards each"),
+        Workload("qwen3-32b_b16_n32768_s32_l64", 7, 16, 64, 8, 64, 32768, 32, "perm",
+                 description="eight query heads per KV head (Qwen3-32B: 64 query / 8 KV heads), "
+                             "64 layers, batch 16, context 32,768, paged, 32 shards"),
         Workload("qwen3-0.6b_b1_n131072_s2_l28_planted", 6, 1, 16, 8, 28, 1 << 17, 2, "perm",
                  planted=True, planted_count=50,
                  description="one GPU's share of the 2^20-position request sharded by position "
