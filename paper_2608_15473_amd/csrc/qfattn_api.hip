@@ -563,7 +563,7 @@ int qf_schedule_simulate(int32_t n_requests, const double* arrival, const double
   const int rc = qf::simulate_schedule(n_requests, arrival, attn_time, n_layers, wiring, ffn_time,
                                        min_batch, max_wait, finish, sweep_start, sweep_end,
                                        ffn_depart, ffn_return);
-  if (rc) return fail(rc, "simulation failed (out of host memory?)");
+  if (rc) return fail(rc, "simulation failed (out of host memory, or no end within its bound on instants)");
   return QF_OK;
 }
 

@@ -9,7 +9,9 @@
 //             joins pool l and starts sweep l+1 (e_1 = arrival + a, finish = ffn_L return).
 //   Composed: the request joins pool l when sweep l ends; sweep l+1 starts when it returns.
 // At each instant all completions (and what they make ready at that same instant) are applied
-// before any pool decides whether to depart.
+// before any pool decides whether to depart.  A pool's time-out instant is computed once, by one
+// expression (deadline()), both where the wake-up is scheduled and where the departure is
+// decided, so the two agree bit for bit for any floating-point times.
 #include <math.h>
 #include <stdint.h>
 
@@ -40,8 +42,12 @@ class Simulation {
     for (int r = 0; r < R; ++r) start_sweep(r, 0, arrival[r]);
   }
 
-  void run() {
+  // false if the run did not end within its bound on instants (it always does: every instant
+  // holds a sweep end, a return, or the wake-up of a pool that departs or frees at that instant).
+  bool run() {
+    int64_t budget = 8 * (int64_t)R_ * L_ + 16;
     while (!events_.empty()) {
+      if (--budget < 0) return false;
       const double t = events_.begin()->first;
       // completions at t, to a fixed point (handlers may add events at t)
       while (!events_.empty() && events_.begin()->first == t) {
@@ -55,9 +61,10 @@ class Simulation {
         if (free_at_[l] > t)
           events_[free_at_[l]];
         else if (isfinite(max_wait_))
-          events_[fmax(waiting_[l].front().first + max_wait_, t)];
+          events_[fmax(deadline(l), t)];
       }
     }
+    return true;
   }
 
   void copy_out(double* finish, double* sweep_start, double* sweep_end, double* depart,
@@ -73,6 +80,9 @@ class Simulation {
 
  private:
   int idx(int r, int l) const { return r * L_ + l; }
+
+  // The instant at which pool l's oldest waiting request has waited max_wait (+inf: never).
+  double deadline(int l) const { return waiting_[l].front().first + max_wait_; }
 
   void start_sweep(int r, int l, double t) {
     sweep_start_[idx(r, l)] = t;
@@ -116,7 +126,7 @@ class Simulation {
   void try_depart(int l, double t) {
     std::deque<std::pair<double, int>>& q = waiting_[l];
     if (q.empty() || free_at_[l] > t) return;
-    if ((int)q.size() < min_batch_ && !(t - q.front().first >= max_wait_)) return;
+    if ((int)q.size() < min_batch_ && !(t >= deadline(l))) return;
     Event e{1, -1, l, {}};
     for (const auto& w : q) {
       e.members.push_back(w.second);
@@ -150,7 +160,7 @@ int simulate_schedule(int R, const double* arrival, const double* attn_time, int
                       double* ffn_return) {
   try {
     Simulation sim(R, arrival, attn_time, L, wiring, ffn_time, min_batch, max_wait);
-    sim.run();
+    if (!sim.run()) return QF_EINVAL;
     sim.copy_out(finish, sweep_start, sweep_end, ffn_depart, ffn_return);
   } catch (...) {
     return QF_EINVAL;
