@@ -13,7 +13,8 @@
  * partition, any order; an empty shard is ln Z = -inf with a vector that is never read).
  *
  * Entry points: the sweep and its merge (qf_attn_decode_split, qf_attn_combine, or both in one
- * launch: qf_attn_decode; qf_attn_decode_split_unfolded leaves sub-shard chunks as extra slots); the decode step
+ * launch: qf_attn_decode, and qf_attn_decode_noalloc for callers that cannot allocate;
+ * qf_attn_decode_split_unfolded leaves sub-shard chunks as extra slots); the decode step
  * around them (qf_attn_combine_current folds in the current token, qf_kv_append writes it to the
  * cache, qf_attn_combine_current_append does both in one launch); the dense products of a decoder block (qf_linear) and the sweep sharing one launch with
  * one of them (qf_attn_decode_split_beside); and a host-side simulation of the layer-wise decode
@@ -23,7 +24,8 @@
  *   - Every pointer argument except `stream` is a DEVICE pointer, owned by the caller, except
  *     where a declaration says HOST (qf_schedule_simulate, the `beside` struct of
  *     qf_attn_decode_split_beside).  The library allocates no memory, keeps no pointer after
- *     returning and holds no per-call state.
+ *     returning and holds no per-call state; the one exception is qf_attn_decode_noalloc, which
+ *     works in a fixed device array of the library's own.
  *   - Every call is asynchronous: it validates its arguments on the host, enqueues its kernels on
  *     `stream` (a hipStream_t; NULL = the legacy default stream) and returns without waiting.
  *   - Return value: QF_OK (0) or a negative QF_E* code.  On error nothing has been enqueued, and
@@ -45,7 +47,7 @@
 extern "C" {
 #endif
 
-#define QF_VERSION 4
+#define QF_VERSION 5
 
 #define QF_OK 0
 #define QF_EINVAL (-1)       /* null pointer, negative or inconsistent size, Hq % Hkv != 0   */
@@ -168,6 +170,33 @@ int qf_attn_decode(const qf_decode_desc* desc, const void* q, const void* k_cach
                    const int32_t* n_shards, void* out, float* lse, void* workspace,
                    size_t workspace_bytes, int32_t* counters, int64_t n_counters,
                    void* stream);
+
+/*
+ * qf_attn_decode for callers that cannot allocate device memory or pass a workspace (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the same sweep and
+ * merge in one launch, with the same results (bitwise) as qf_attn_decode on the same inputs, but
+ * the partial states and the per-(request, KV head) counters live in a fixed device array of the
+ * library's own, QF_NOALLOC_SCRATCH_BYTES (64 MiB) on every GPU the library runs on, held until the
+ * process ends.  The call allocates nothing; it enqueues a small kernel that clears the counters
+ * it will use, then the decode.
+ *
+ *   q ... n_shards, out, lse   as for qf_attn_decode.
+ *   stream                     hipStream_t of the CURRENT device (the scratch used is the current
+ *                              device's; its address is looked up on the first call there).
+ * Limits: the shape's qf_attn_decode_workspace_size() must be at most QF_NOALLOC_STATE_BYTES and
+ * batch * n_kv_heads at most QF_NOALLOC_MAX_GROUPS; otherwise QF_EINVAL, with nothing enqueued.
+ * Every call on a GPU shares that GPU's array, whose contents are left from the last call: calls
+ * that may overlap on one GPU (concurrent streams, or host threads) race and give wrong results;
+ * serialise them (one stream), or use qf_attn_decode with a workspace and counters per stream.
+ * Returns the codes of qf_attn_decode; QF_EHIP also when the array's address cannot be found.
+ */
+#define QF_NOALLOC_SCRATCH_BYTES (64u << 20)
+#define QF_NOALLOC_STATE_BYTES ((64u << 20) - (256u << 10))
+#define QF_NOALLOC_MAX_GROUPS 65536
+int qf_attn_decode_noalloc(const qf_decode_desc* desc, const void* q, const void* k_cache,
+                           const void* v_cache, const int32_t* block_table,
+                           const int32_t* ctx_lens, const int32_t* n_shards, void* out,
+                           float* lse, void* stream);
 
 /*
  * The merge of §5 over every shard slot: for each request b and query head h,

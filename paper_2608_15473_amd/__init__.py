@@ -27,6 +27,7 @@ from .binding import (  # noqa: F401
     attn_combine_current,
     attn_combine_current_append,
     attn_decode,
+    attn_decode_noalloc,
     attn_decode_split,
     attn_decode_split_beside,
     attn_decode_split_unfolded,

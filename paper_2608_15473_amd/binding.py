@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "lib", "libqfattn.so")
 QF_OK, QF_EINVAL, QF_EUNSUPPORTED, QF_EALIGN, QF_EHIP = 0, -1, -2, -3, -4
 EXPORTED = ("qf_attn_decode_split_workspace_size", "qf_attn_decode_split", "qf_attn_combine",
             "qf_attn_decode_split_chunks", "qf_attn_decode_split_unfolded",
-            "qf_attn_decode_workspace_size", "qf_attn_decode",
+            "qf_attn_decode_workspace_size", "qf_attn_decode", "qf_attn_decode_noalloc",
             "qf_attn_combine_current", "qf_attn_combine_current_append", "qf_kv_append",
             "qf_linear", "qf_attn_decode_split_beside",
             "qf_schedule_simulate", "qf_last_error", "qf_version")
@@ -72,6 +72,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.qf_attn_decode_workspace_size.argtypes = [ctypes.POINTER(DecodeDesc), ctypes.POINTER(sz)]
     lib.qf_attn_decode.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                    sz, vp, ctypes.c_int64, vp]
+    lib.qf_attn_decode_noalloc.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp, vp, vp,
+                                           vp, vp]
     lib.qf_attn_combine_current.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, vp,
                                             ctypes.c_float, vp, vp, vp]
     lib.qf_attn_combine_current_append.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp,
@@ -89,7 +91,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.qf_version.argtypes = []
     for name in ("qf_attn_decode_split_workspace_size", "qf_attn_decode_split",
                  "qf_attn_decode_split_chunks", "qf_attn_decode_split_unfolded",
-                 "qf_attn_decode_workspace_size", "qf_attn_decode",
+                 "qf_attn_decode_workspace_size", "qf_attn_decode", "qf_attn_decode_noalloc",
                  "qf_attn_combine", "qf_attn_combine_current", "qf_attn_combine_current_append",
                  "qf_kv_append",
                  "qf_linear", "qf_attn_decode_split_beside", "qf_schedule_simulate", "qf_version"):
@@ -527,6 +529,45 @@ def attn_decode(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards
         ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
         _ptr(ctx_lens), _ptr(n_shards), _ptr(out), _ptr(lse), _ptr(workspace),
         workspace.numel(), _ptr(counters), counters.numel(), ctypes.c_void_p(stream)))
+    return out, lse
+
+
+def attn_decode_noalloc(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards=None,
+                        scale=None, out=None, lse=None, max_pages=None, want_lse=True):
+    """``attn_decode`` without a workspace or counters (qf_attn_decode_noalloc): the library works
+    in its own fixed device array, so the call allocates nothing on the device (``out`` / ``lse``
+    and an int ``n_shards`` are still made here when not given).  Calls that may overlap on one
+    GPU race on that array.  Returns (out bf16 [B, Hq, D], lse fp32 [B, Hq])."""
+    _require(q, "q", torch.bfloat16, 3)
+    _require(k_cache, "k_cache", torch.bfloat16, 4)
+    _require(v_cache, "v_cache", torch.bfloat16, 4)
+    if v_cache.shape != k_cache.shape:
+        raise QFError(QF_EINVAL, "k_cache and v_cache shapes differ")
+    if block_table is not None:
+        _require(block_table, "block_table", torch.int32, 2)
+    _require(ctx_lens, "ctx_lens", torch.int32, 1)
+    B, Hq, D = q.shape
+    if isinstance(n_shards, int):
+        if max_shards is None:
+            max_shards = n_shards
+        n_shards = torch.full((B,), n_shards, dtype=torch.int32, device=q.device)
+    _require(n_shards, "n_shards", torch.int32, 1)
+    if max_shards is None:
+        raise QFError(QF_EINVAL, "max_shards is required when n_shards is a tensor")
+    if scale is None:
+        scale = D ** -0.5
+    desc = make_desc(q, k_cache, block_table, max_shards, scale, max_pages=max_pages)
+    if out is None:
+        out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=q.device)
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
+    _require(out, "out", torch.bfloat16)
+    if out.numel() != B * Hq * D or (lse is not None and lse.numel() != B * Hq):
+        raise QFError(QF_EINVAL, "out / lse sizes do not match q")
+    stream = torch.cuda.current_stream(q.device).cuda_stream
+    _check(load_library().qf_attn_decode_noalloc(
+        ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+        _ptr(ctx_lens), _ptr(n_shards), _ptr(out), _ptr(lse), ctypes.c_void_p(stream)))
     return out, lse
 
 

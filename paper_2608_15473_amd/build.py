@@ -14,8 +14,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIBDIR = os.path.join(PKG, "lib")
 LIB = os.path.join(LIBDIR, "libqfattn.so")
-SOURCES = ["qfattn_api.hip", "decode_split.hip", "merge.hip", "kv_append.hip", "block_ops.hip",
-           "schedule.cpp"]
+SOURCES = ["qfattn_api.hip", "decode_split.hip", "decode_noalloc.hip", "merge.hip", "kv_append.hip",
+           "block_ops.hip", "schedule.cpp"]
 ARCH = "gfx950"
 
 # Packed-FP32 instructions are disabled for every HIP translation unit; hipcc's host pass does not

@@ -113,6 +113,16 @@ int simulate_schedule(int R, const double* arrival, const double* attn_time, int
 
 hipError_t launch_decode_split(const SplitParams& p, int group, hipStream_t stream);
 
+// The allocation-free decode's fixed scratch (decode_noalloc.hip): one device array per GPU of
+// kNoallocScratchBytes, the counters in its first kNoallocCounterBytes, the partial states after.
+constexpr size_t kNoallocScratchBytes = size_t(64) << 20;
+constexpr size_t kNoallocCounterBytes = size_t(256) << 10;
+constexpr size_t kNoallocStateBytes = kNoallocScratchBytes - kNoallocCounterBytes;
+// This device's scratch (looked up on the first call on the device): *counters (n_counters int32
+// entries, cleared to zero on `stream` before anything else is enqueued there) and *states.
+hipError_t noalloc_prepare(int32_t n_counters, hipStream_t stream, int32_t** counters,
+                           void** states);
+
 // Workgroups of the long-shard sweep (kSplitBuffers) at group size `group` that are resident on
 // the current device at once (compute units x workgroups per unit); 0 when there is no device to
 // ask.  Queried once per group size and kept.

@@ -241,6 +241,13 @@ int prepare_linear(const qf_linear_args* a, qf::LinearParams* out_p, bool* noop)
   return QF_OK;
 }
 
+// The one-launch decode on a given workspace and counters (qf_attn_decode's body; defined below).
+int decode_fused(const qf_decode_desc* desc, const void* q, const void* k_cache,
+                 const void* v_cache, const int32_t* block_table, const int32_t* ctx_lens,
+                 const int32_t* n_shards, void* out, float* lse, void* workspace,
+                 size_t workspace_size, int32_t* counters, int64_t n_counters, void* stream,
+                 bool fixed_scratch);
+
 }  // namespace
 
 extern "C" {
@@ -313,36 +320,90 @@ int qf_attn_decode(const qf_decode_desc* desc, const void* q, const void* k_cach
                    const int32_t* n_shards, void* out, float* lse, void* workspace,
                    size_t workspace_size, int32_t* counters, int64_t n_counters, void* stream) {
   g_error[0] = 0;
+  return decode_fused(desc, q, k_cache, v_cache, block_table, ctx_lens, n_shards, out, lse,
+                      workspace, workspace_size, counters, n_counters, stream, false);
+}
+
+int qf_attn_decode_noalloc(const qf_decode_desc* desc, const void* q, const void* k_cache,
+                           const void* v_cache, const int32_t* block_table,
+                           const int32_t* ctx_lens, const int32_t* n_shards, void* out,
+                           float* lse, void* stream) {
+  g_error[0] = 0;
+  return decode_fused(desc, q, k_cache, v_cache, block_table, ctx_lens, n_shards, out, lse,
+                      nullptr, 0, nullptr, 0, stream, true);
+}
+
+}  // extern "C"
+
+namespace {
+
+// fixed_scratch: workspace and counters are the library's own scratch array (decode_noalloc.hip),
+// looked up and its counters cleared only once every argument has passed its checks, so that a
+// refused call enqueues nothing.
+int decode_fused(const qf_decode_desc* desc, const void* q, const void* k_cache,
+                 const void* v_cache, const int32_t* block_table, const int32_t* ctx_lens,
+                 const int32_t* n_shards, void* out, float* lse, void* workspace,
+                 size_t workspace_size, int32_t* counters, int64_t n_counters, void* stream,
+                 bool fixed_scratch) {
   int rc = check_desc(desc);
   if (rc) return rc;
   const qf_decode_desc& d = *desc;
   if (d.batch == 0) return QF_OK;
-  if (!out || !workspace || !counters)
+  const int64_t chunks = choose_chunks(&d);
+  const size_t need = fused_workspace_bytes(&d, chunks);
+  const int64_t groups = (int64_t)d.batch * d.n_kv_heads;
+  if (fixed_scratch) {
+    // Sizes first: a shape beyond the fixed scratch is refused before anything touches the GPU.
+    const int64_t max_groups = (int64_t)(qf::kNoallocCounterBytes / sizeof(int32_t));
+    if (need > qf::kNoallocStateBytes || groups > max_groups)
+      return fail(QF_EINVAL,
+                  "shape needs %zu bytes of partial states and %lld (request, KV head) counters; "
+                  "the fixed scratch holds %zu bytes and %lld counters (qf_attn_decode takes a "
+                  "workspace of any size)",
+                  need, (long long)groups, qf::kNoallocStateBytes, (long long)max_groups);
+    // Placeholders (aligned, never dereferenced) until the arguments have been checked.
+    workspace = reinterpret_cast<void*>(uintptr_t(256));
+    workspace_size = need;
+    counters = reinterpret_cast<int32_t*>(uintptr_t(256));
+    n_counters = groups;
+    if (!out) return fail(QF_EINVAL, "out is required");
+  } else if (!out || !workspace || !counters) {
     return fail(QF_EINVAL, "out, workspace and counters are required");
-  if (n_counters < (int64_t)d.batch * d.n_kv_heads)
+  }
+  if (n_counters < groups)
     return fail(QF_EINVAL, "counters holds %lld entries < batch * n_kv_heads = %lld",
-                (long long)n_counters, (long long)d.batch * d.n_kv_heads);
+                (long long)n_counters, (long long)groups);
   if (!aligned(out, 4) || (lse && !aligned(lse, 4)) || !aligned(workspace, 16) ||
       !aligned(counters, 4))
     return fail(QF_EALIGN, "out, lse and counters must be 4-byte aligned, workspace 16-byte");
-  const int64_t chunks = choose_chunks(&d);
-  const size_t need = fused_workspace_bytes(&d, chunks);
   if (workspace_size < need)
     return fail(QF_EINVAL, "workspace of %zu bytes < %zu needed", workspace_size, need);
   // The partial states live in the workspace, seen by the sweep as its per-slot outputs (with
   // chunks == 1 its direct outputs, otherwise its chunk states): one layout [B, S x C, Hq, .].
-  float* states = static_cast<float*>(workspace);
   const size_t n_states = (size_t)d.batch * d.max_shards * chunks * d.n_q_heads;
+  float* states = static_cast<float*>(workspace);
   Split sp;
   rc = prepare_split(desc, q, k_cache, v_cache, block_table, ctx_lens, n_shards, states,
                      states + n_states * qf::kHeadDim, chunks > 1 ? workspace : nullptr,
                      chunks > 1 ? need : 0, &sp);
   if (rc || sp.noop) return rc;
-  const hipError_t e = qf::launch_decode_fused(sp.p, sp.group, counters, out, lse,
-                                               static_cast<hipStream_t>(stream));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (fixed_scratch) {
+    void* base = nullptr;
+    const hipError_t e = qf::noalloc_prepare((int32_t)groups, s, &counters, &base);
+    if (e != hipSuccess) return fail(QF_EHIP, "scratch set-up: %s", hipGetErrorString(e));
+    states = static_cast<float*>(base);
+    sp.p.out_o = states;
+    sp.p.out_lse = states + n_states * qf::kHeadDim;
+  }
+  const hipError_t e = qf::launch_decode_fused(sp.p, sp.group, counters, out, lse, s);
   if (e != hipSuccess) return fail(QF_EHIP, "decode launch: %s", hipGetErrorString(e));
   return QF_OK;
 }
+
+}  // namespace
+
+extern "C" {
 
 int qf_attn_combine(int32_t batch, int32_t n_q_heads, int32_t head_dim, int32_t max_shards,
                     const float* part_out, const float* part_lse, void* out, float* lse,
