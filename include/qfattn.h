@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define QF_VERSION 5
+#define QF_VERSION 6
 
 #define QF_OK 0
 #define QF_EINVAL (-1)       /* null pointer, negative or inconsistent size, Hq % Hkv != 0   */
@@ -130,15 +130,18 @@ int qf_attn_decode_split_chunks(const qf_decode_desc* desc, int32_t* chunks);
  * workspace: for callers that need only the merged attention, not per-shard partials.
  *
  *   q ... n_shards   as for qf_attn_decode_split.
- *   slot_out    fp32 [B, max_shards * C, Hq, D], 16-byte aligned: O of every non-empty chunk.
- *   slot_lse    fp32 [B, max_shards * C, Hq], 4-byte aligned: ln Z of every chunk slot; -inf for
- *               an empty chunk and for every chunk of a slot s >= S_b; NaN as for part_lse.
+ *   slot_out    fp32 [B, n_slots, Hq, D], 16-byte aligned: O of every non-empty chunk.
+ *   slot_lse    fp32 [B, n_slots, Hq], 4-byte aligned: ln Z of every chunk slot; -inf for an
+ *               empty chunk and for every chunk of a slot s >= S_b; NaN as for part_lse.
+ *   n_slots     the slot dimension of slot_out and slot_lse: must equal max_shards * C
+ *               (QF_EINVAL otherwise, with nothing enqueued).
  *   stream      hipStream_t.
  */
 int qf_attn_decode_split_unfolded(const qf_decode_desc* desc, const void* q, const void* k_cache,
                                   const void* v_cache, const int32_t* block_table,
                                   const int32_t* ctx_lens, const int32_t* n_shards,
-                                  float* slot_out, float* slot_lse, void* stream);
+                                  float* slot_out, float* slot_lse, int32_t n_slots,
+                                  void* stream);
 
 /*
  * The sweep and the merge in ONE launch: the result of qf_attn_decode_split followed by

@@ -68,7 +68,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.qf_attn_decode_split_chunks.argtypes = [ctypes.POINTER(DecodeDesc),
                                                 ctypes.POINTER(ctypes.c_int32)]
     lib.qf_attn_decode_split_unfolded.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp,
-                                                  vp, vp, vp, vp]
+                                                  vp, vp, vp, i32, vp]
     lib.qf_attn_decode_workspace_size.argtypes = [ctypes.POINTER(DecodeDesc), ctypes.POINTER(sz)]
     lib.qf_attn_decode.argtypes = [ctypes.POINTER(DecodeDesc), vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                    sz, vp, ctypes.c_int64, vp]
@@ -185,7 +185,7 @@ def _split_call(q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards
     head = (ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
             _ptr(ctx_lens), _ptr(n_shards), _ptr(part_out), _ptr(part_lse))
     if unfolded:
-        return head, desc, part_out, part_lse, None, n_shards
+        return head + (slots,), desc, part_out, part_lse, None, n_shards
     need = workspace_size(desc)
     if need and workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)

@@ -482,17 +482,26 @@ swept:
   __shared__ float s_acc[W][G][D];
   __shared__ float s_m[W][G];
   __shared__ float s_l[W][G];
+  __shared__ int s_bad[W];
   if (row == 0) {
 #pragma unroll
     for (int h = 0; h < G; ++h)
 #pragma unroll
       for (int e = 0; e < 8; ++e) s_acc[wave][h][col * 8 + e] = acc[h][e];
   }
+  // Any poisoned wavefront poisons the unit: a ballot per wavefront, met in LDS at the barrier
+  // the merge needs anyway (cheaper in registers than __syncthreads_or, which rebuilds a flat
+  // thread index from the y and z indices).
+  const bool wave_bad = __builtin_amdgcn_ballot_w64(poison) != 0;
   if (lane == 0) {
 #pragma unroll
     for (int h = 0; h < G; ++h) { s_m[wave][h] = m[h]; s_l[wave][h] = l[h]; }
+    s_bad[wave] = wave_bad ? 1 : 0;
   }
-  const int bad = __syncthreads_or(poison ? 1 : 0);
+  __syncthreads();
+  int bad = 0;
+#pragma unroll
+  for (int w = 0; w < W; ++w) bad |= s_bad[w];
 
   const size_t slot = (((size_t)b * max_shards + s) * chunks + c) * hq + (size_t)g * G;
   for (int idx = threadIdx.x; idx < G * D; idx += 64 * W) {

@@ -77,14 +77,21 @@ __device__ __forceinline__ void merge_row(
                   : -INFINITY;
       else
         x[k] = in ? lse[(size_t)(i0 + k) * hq] : -INFINITY;
+    }
+    // O only where the slot holds positions: most slots of a ragged batch are empty, and their
+    // O (never written) is not worth a read.
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const bool live = x[k] != -INFINITY;
       if (COHERENT) {
         const float* of = reinterpret_cast<const float*>(o + (size_t)(i0 + k) * o_step);
-        v[k] = in ? make_float2(__hip_atomic_load(of, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
-                                __hip_atomic_load(of + 1, __ATOMIC_RELAXED,
-                                                  __HIP_MEMORY_SCOPE_AGENT))
-                  : make_float2(0.0f, 0.0f);
+        v[k] = live ? make_float2(__hip_atomic_load(of, __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT),
+                                  __hip_atomic_load(of + 1, __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT))
+                    : make_float2(0.0f, 0.0f);
       } else {
-        v[k] = in ? o[(size_t)(i0 + k) * o_step] : make_float2(0.0f, 0.0f);
+        v[k] = live ? o[(size_t)(i0 + k) * o_step] : make_float2(0.0f, 0.0f);
       }
     }
     float mc = m_w;

@@ -292,14 +292,25 @@ int qf_attn_decode_split_chunks(const qf_decode_desc* desc, int32_t* chunks) {
 int qf_attn_decode_split_unfolded(const qf_decode_desc* desc, const void* q, const void* k_cache,
                                   const void* v_cache, const int32_t* block_table,
                                   const int32_t* ctx_lens, const int32_t* n_shards,
-                                  float* slot_out, float* slot_lse, void* stream) {
+                                  float* slot_out, float* slot_lse, int32_t n_slots,
+                                  void* stream) {
   g_error[0] = 0;
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  if (desc->batch == 0) return QF_OK;
+  // The slot count of the caller's arrays, checked against the one the sweep writes (it depends on
+  // the device's resident workgroups, so a caller sizing by max_shards alone would be overrun).
+  const int64_t want = (int64_t)desc->max_shards * choose_chunks(desc);
+  if (want > (int64_t)INT32_MAX) return fail(QF_EINVAL, "max_shards * chunks exceeds int32");
+  if (n_slots != want)
+    return fail(QF_EINVAL,
+                "the slot arrays hold %d slots per request; this shape needs %lld (max_shards x "
+                "qf_attn_decode_split_chunks)",
+                n_slots, (long long)want);
   Split sp;
-  const int rc = prepare_split(desc, q, k_cache, v_cache, block_table, ctx_lens, n_shards,
-                               slot_out, slot_lse, nullptr, 0, &sp, false);
+  rc = prepare_split(desc, q, k_cache, v_cache, block_table, ctx_lens, n_shards, slot_out,
+                     slot_lse, nullptr, 0, &sp, false);
   if (rc || sp.noop) return rc;
-  if ((int64_t)desc->max_shards * sp.chunks > (int64_t)INT32_MAX)
-    return fail(QF_EINVAL, "max_shards * chunks exceeds int32");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const hipError_t e = qf::launch_decode_split(sp.p, sp.group, s);
   if (e != hipSuccess) return fail(QF_EHIP, "decode_split launch: %s", hipGetErrorString(e));

@@ -331,9 +331,23 @@ def test_unfolded_sweep_rejects_before_launch():
     a = ctypes.c_void_p(4096)
     fn = lib.qf_attn_decode_split_unfolded
     d = _desc()
-    assert fn(ctypes.byref(d), a, a, a, None, a, a, a, None, None) == qf.QF_EINVAL
-    assert fn(ctypes.byref(d), ctypes.c_void_p(4098), a, a, None, a, a, a, a, None) == qf.QF_EALIGN
+    c = ctypes.c_int32(0)
+    assert lib.qf_attn_decode_split_chunks(ctypes.byref(d), ctypes.byref(c)) == qf.QF_OK
+    slots = d.max_shards * c.value
+    assert fn(ctypes.byref(d), a, a, a, None, a, a, a, None, slots, None) == qf.QF_EINVAL
+    assert fn(ctypes.byref(d), ctypes.c_void_p(4098), a, a, None, a, a, a, a, slots,
+              None) == qf.QF_EALIGN
+    # slot arrays sized for another chunk count (e.g. by max_shards alone on a chunked shape):
+    # refused before anything is enqueued
+    for wrong in (slots - 1, slots + 1, d.max_shards if c.value > 1 else 0):
+        assert fn(ctypes.byref(d), a, a, a, None, a, a, a, a, wrong, None) == qf.QF_EINVAL
+        assert "slots" in lib.qf_last_error().decode()
+    chunked = _desc(batch=1, max_shards=16, max_pages_per_seq=65536, num_pages=65536)
+    assert lib.qf_attn_decode_split_chunks(ctypes.byref(chunked), ctypes.byref(c)) == qf.QF_OK
+    assert c.value > 1
+    assert fn(ctypes.byref(chunked), a, a, a, None, a, a, a, a, 16, None) == qf.QF_EINVAL
     bad = _desc(head_dim=64)
-    assert fn(ctypes.byref(bad), a, a, a, None, a, a, a, a, None) == qf.QF_EUNSUPPORTED
+    assert fn(ctypes.byref(bad), a, a, a, None, a, a, a, a, slots, None) == qf.QF_EUNSUPPORTED
     empty = _desc(batch=0)
-    assert fn(ctypes.byref(empty), None, None, None, None, None, None, None, None, None) == qf.QF_OK
+    assert fn(ctypes.byref(empty), None, None, None, None, None, None, None, None, 0,
+              None) == qf.QF_OK

@@ -1,0 +1,124 @@
+"""GPU parity of ragged batches with long shards against the fp64 oracle.
+
+Shapes with many (request, shard, KV head) units whose shards are long (128+ pages per shard at full
+capacity) are swept largest shard first, one workgroup per unit.  Every output of every case is
+checked: per-shard partials and the combined result, at every group size, including requests with
+no positions, partial last pages, more shards than pages, very little work in all, one long request
+next to many short ones, out-of-range device values, and the unfolded sweep (chunks left as slots)
+followed by the combine."""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_15473_amd as qf
+from parity import check, oracle_ref, run_gpu, say
+from workloads import make_case
+
+pytestmark = pytest.mark.gpu
+
+
+def _desc(case):
+    return qf.make_desc(case.q, case.k_cache, case.block_table, case.max_shards, case.scale)
+
+
+def _is_long_shard_shape(case):
+    """128+ pages per shard at full capacity and at least one full set of resident workgroups'
+    worth of units (no sub-shard chunks)."""
+    B, S = case.q.shape[0], case.max_shards
+    long = -(-case.block_table.shape[1] // S) >= 128
+    return long and qf.split_chunks(_desc(case)) == 1
+
+
+def _ragged(batch, seed, n_max=40000):
+    rng = np.random.default_rng(seed)
+    n = np.rint(np.exp(rng.uniform(np.log(8), np.log(n_max), size=batch))).astype(int)
+    n[[1, 7]] = 0                       # no positions
+    n[2] = 1                            # one position
+    n[3] = 16 * 37 + 5                  # partial last page
+    S = np.maximum(1, -(-n // 4096))
+    S[4] = 16                           # more shards than it has pages for some of them
+    n[4] = 16 * 9 + 3
+    return n, S
+
+
+@pytest.mark.parametrize("G", [1, 2, 4, 8])
+def test_long_shards_every_group_size(gpu, G):
+    n, S = _ragged(48, 400 + G)
+    case = make_case(48, 2 * G, 2, n, S, seed=400 + G, max_shards=16, max_pages=2560, device=gpu)
+    assert _is_long_shard_shape(case), "the shape must be a long-shard, unchunked one"
+    say(f"[long shards] G={G}: {int(n.sum())} positions")
+    got = run_gpu(case)
+    ref = oracle_ref(case)
+    worst = check(case, got, ref, label=f"long shards G={G}")
+    say(f"[long shards] G={G}: ok {worst}")
+    assert np.all(got["part_lse"][[1, 7]] == -np.inf)
+    for b in range(48):
+        assert np.all(got["part_lse"][b, S[b]:] == -np.inf)
+
+
+def test_long_shards_with_little_work(gpu):
+    """Few pages in all (most units empty or of a few pages), and one request whose single shard
+    is 100 times longer than the others."""
+    n = np.full(64, 40)
+    n[5] = 16 * 300 + 7                         # one shard of 301 pages
+    S = np.ones(64, dtype=int)
+    S[9] = 3
+    case = make_case(64, 16, 8, n, S, seed=420, max_shards=4, max_pages=1024, device=gpu)
+    assert _is_long_shard_shape(case)
+    say("[long shards] little work")
+    got = run_gpu(case)
+    check(case, got, oracle_ref(case), label="long shards, little work")
+
+
+def test_long_shards_poison_out_of_range_requests(gpu):
+    n, S = _ragged(48, 430)
+    case = make_case(48, 16, 2, n, S, seed=430, max_shards=16, max_pages=2560, device=gpu)
+    assert _is_long_shard_shape(case)
+    heavy = int(np.argmax(n))
+    case.block_table[heavy, 5] = case.k_cache.shape[0] + 3     # entry past the pool
+    case.ctx_lens[10] = 10**7                                  # past the table row
+    case.n_shards[11] = 999                                    # more shards than slots
+    case.ctx_lens[12] = -1
+    say("[long shards] poisoned requests")
+    got = run_gpu(case)
+    for b in (heavy, 10, 11, 12):
+        assert np.all(np.isnan(got["lse"][b])), b
+    assert np.all(np.isnan(got["part_lse"][12]))
+    good = [b for b in range(48) if b not in (heavy, 10, 11, 12)]
+    pairs = [(b, h) for b in good[::5] for h in (0, 7)]
+    ref = make_case(48, 16, 2, n, S, seed=430, max_shards=16, max_pages=2560, device=gpu)
+    check(ref, got, oracle_ref(ref, pairs), pairs, label="long shards, poison/others")
+
+
+def test_long_shards_unfolded_then_combine(gpu):
+    """The unfolded sweep followed by the combine (no chunks here, so the slots are the shards)
+    equals the split sweep followed by the combine bitwise, and the oracle's gates."""
+    n, S = _ragged(48, 440)
+    case = make_case(48, 32, 8, n, S, seed=440, max_shards=16, max_pages=2560, device=gpu)
+    assert _is_long_shard_shape(case)
+    C = qf.split_chunks(_desc(case))
+    args = (case.q, case.k_cache, case.v_cache, case.block_table, case.ctx_lens, case.n_shards)
+    so = torch.full((48, 16 * C, 32, 128), float("nan"), device=gpu)
+    sl = torch.full((48, 16 * C, 32), float("nan"), device=gpu)
+    qf.attn_decode_split_unfolded(*args, max_shards=16, scale=case.scale, slot_out=so,
+                                  slot_lse=sl)
+    out, lse = qf.attn_combine(so, sl)
+    folded = run_gpu(case)
+    torch.cuda.synchronize()
+    say("[long shards] unfolded")
+    assert not torch.isnan(sl).any()
+    assert np.array_equal(lse.cpu().numpy(), folded["lse"])
+    assert np.array_equal(out.view(torch.int16).cpu().numpy(), folded["out_bits"])
+    got = dict(folded)
+    got["out"], got["lse"] = out.float().cpu().numpy(), lse.cpu().numpy()
+    got["out_bits"] = out.view(torch.int16).cpu().numpy()
+    check(case, got, oracle_ref(case), label="long shards, unfolded")
+
+
+def test_long_shards_are_deterministic(gpu):
+    n, S = _ragged(48, 450)
+    case = make_case(48, 16, 2, n, S, seed=450, max_shards=16, max_pages=2560, device=gpu)
+    a, b = run_gpu(case), run_gpu(case)
+    for key in ("part_out", "part_lse", "out_bits", "lse"):
+        assert np.array_equal(a[key], b[key], equal_nan=True), key
