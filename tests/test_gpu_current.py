@@ -58,7 +58,7 @@ def _fold_reference(case, k_new, v_new):
                                v_new.double().cpu().numpy(), case.scale)
 
 
-@pytest.mark.parametrize("Hq,Hkv", [(16, 8), (32, 8), (8, 8)])
+@pytest.mark.parametrize("Hq,Hkv", [(16, 8), (32, 8), (8, 8), (64, 8)])
 def test_fold_current_matches_oracle(gpu, Hq, Hkv):
     case = _allocated_case(gpu, 4, Hq, Hkv, [700, 1, 0, 2100], [3, 1, 2, 5], seed=200 + Hq)
     k_new, v_new = _new_token(case, 201)

@@ -15,6 +15,7 @@ import torch
 import torch.nn.functional as F
 
 import oracle
+from oracle import block as oracle_block
 from workloads import BlockShape, block_input, block_weights
 
 SHAPE = BlockShape("tiny", hidden=64, inter=96, n_q_heads=4, n_kv_heads=2, layers=1)
@@ -167,3 +168,48 @@ def test_stepwise_decode_equals_causal_attention_over_the_sequence(T):
                                        enable_gqa=True)                # [Hq, T, D]
     Y = Z + F.linear(A.transpose(0, 1).reshape(T, -1), W["w_o"])
     np.testing.assert_allclose(np.stack(ys), Y.numpy(), rtol=1e-11, atol=1e-12)
+
+
+def test_round_bf16_matches_torch_conversion():
+    """The oracle's bf16 rounding (nearest float32, then nearest bf16, ties to even) against
+    torch's float32 -> bfloat16 conversion, an independent library routine: random values over
+    many binades, exact ties (the low 16 bits exactly 0x8000, both parities), subnormals, the
+    largest finite values (which round to inf), infinities and NaN."""
+    import torch
+    rng = np.random.default_rng(11)
+    vals = [rng.standard_normal(20000) * 10.0 ** rng.uniform(-40, 38, 20000)]
+    base = rng.integers(0, 1 << 15, 4000, dtype=np.uint64) << np.uint64(16)
+    ties = (base | np.uint64(0x8000)) | (rng.integers(0, 2, 4000, dtype=np.uint64) << np.uint64(31))
+    vals.append(ties.astype(np.uint32).view(np.float32).astype(np.float64))
+    vals.append(np.array([1e-40, -3e-45, 3.3895e38, -3.39e38, np.inf, -np.inf, 0.0, -0.0]))
+    x = np.concatenate(vals)
+    ref = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+    got = oracle_block.round_bf16(x)
+    assert np.array_equal(got, ref, equal_nan=True)
+    assert np.isnan(oracle_block.round_bf16(np.array([np.nan])))[0]
+
+
+def test_block_with_bf16_stores_is_the_exact_block_rounded():
+    """With bf16_stores the seven stored tensors are bf16 values, the rest of the block follows
+    from them exactly, and the output stays within the rounding's reach of the exact block."""
+    B, H, I, Hq, Hkv, D = 3, 64, 96, 4, 2, 16
+    rng = np.random.default_rng(12)
+    w = {"w_q": rng.standard_normal((Hq * D, H)) / 8, "w_k": rng.standard_normal((Hkv * D, H)) / 8,
+         "w_v": rng.standard_normal((Hkv * D, H)) / 8, "w_o": rng.standard_normal((H, Hq * D)) / 8,
+         "w_gate": rng.standard_normal((I, H)) / 8, "w_up": rng.standard_normal((I, H)) / 8,
+         "w_down": rng.standard_normal((H, I)) / 10, "g1": rng.uniform(0.5, 1.5, H),
+         "g2": rng.uniform(0.5, 1.5, H)}
+    u = rng.standard_normal((B, H))
+    kc = rng.standard_normal((6, Hkv, 16, D))
+    vc = rng.standard_normal((6, Hkv, 16, D))
+    bt = np.arange(6).reshape(3, 2)
+    n = np.array([20, 0, 31])
+    exact = oracle_block.qfirst_block(u, w, kc, vc, bt, n, Hq, Hkv, D ** -0.5)
+    emu = oracle_block.qfirst_block(u, w, kc, vc, bt, n, Hq, Hkv, D ** -0.5, bf16_stores=True)
+    for key in ("q", "act", "z", "k", "v", "attn", "y"):
+        assert np.array_equal(oracle_block.round_bf16(emu[key]), emu[key]), key
+    # the first stored tensors are the exact ones rounded (nothing upstream was rounded)
+    assert np.array_equal(emu["q"], oracle_block.round_bf16(exact["q"]))
+    assert np.array_equal(emu["act"], oracle_block.round_bf16(exact["act"]))
+    rel = np.linalg.norm(emu["y"] - exact["y"]) / np.linalg.norm(exact["y"])
+    assert 0 < rel < 2.0 ** -7
