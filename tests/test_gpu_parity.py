@@ -316,11 +316,31 @@ def test_full_size_workload_layer(gpu, name):
         order = np.argsort(n)
         pairs = [(int(order[0]), 3), (int(order[32]), 17), (int(order[-1]), 30)]
     got, ref = _run(case, f"{name} layer {layer}", pairs)
+    got_u = _bench_configuration(case, got, ref, pairs, f"{name} layer {layer}")
     if WORKLOADS[name].planted:
-        assert np.all(np.isfinite(got["out"])) and np.all(np.isfinite(got["lse"]))
-        assert np.all(got["lse"] > 88.0)
+        for g in (got, got_u):
+            assert np.all(np.isfinite(g["out"])) and np.all(np.isfinite(g["lse"]))
+            assert np.all(g["lse"] > 88.0)
     del case
     torch.cuda.empty_cache()
+
+
+def _bench_configuration(case, got, ref, pairs, label):
+    """The launch configuration the bench times (DecodeStepPlan(fold_chunks=False): the sweep
+    leaves sub-shard chunks as slots, one combine merges the max_shards * C of them), gated against
+    the same oracle values as the split sweep and combine."""
+    args = (case.q, case.k_cache, case.v_cache, case.block_table, case.ctx_lens, case.n_shards)
+    plan = qf.DecodeStepPlan(*args, max_shards=case.max_shards, scale=case.scale,
+                             fold_chunks=False)
+    out, lse = plan()
+    torch.cuda.synchronize()
+    got_u = dict(got)
+    got_u["out"], got_u["lse"] = out.float().cpu().numpy(), lse.cpu().numpy()
+    got_u["out_bits"] = out.view(torch.int16).cpu().numpy()
+    worst = check(case, got_u, ref, pairs, label + " (bench configuration)")
+    say(f"[parity] {label} (bench configuration, {plan.part_lse.shape[1]} slots): ok {worst}")
+    del plan
+    return got_u
 
 
 @pytest.mark.slow
@@ -350,10 +370,12 @@ def test_full_size_every_layer_sampled(gpu, name):
         case = workload_case(name, layer=layer, device=gpu)
         B, Hq = case.shape[0], case.shape[1]
         pair = ((7 * layer + 3) % B, (5 * layer + 1) % Hq)
-        got, _ = _run(case, f"{name} layer {layer}", [pair])
+        got, ref = _run(case, f"{name} layer {layer}", [pair])
+        got_u = _bench_configuration(case, got, ref, [pair], f"{name} layer {layer}")
         if w.planted:
-            assert np.all(np.isfinite(got["out"])) and np.all(got["lse"] > 88.0)
-        del case, got
+            for g in (got, got_u):
+                assert np.all(np.isfinite(g["out"])) and np.all(g["lse"] > 88.0)
+        del case, got, got_u
         torch.cuda.empty_cache()
 
 
