@@ -8,7 +8,7 @@ What it computes follows the paper (Q-First, arXiv:2608.15473):
 
 * §2 (the decode protocol): the cache-side device receives only the query and returns the
   attention vector over the cached positions together with its log-sum-exp.
-* §5 ("The cache may be split anywhere"): for a set S of positions with scores s_i and values
+* §5 (splitting the cache): for a set S of positions with scores s_i and values
   v_i, Z(S) = sum_i exp(s_i), W(S) = sum_i exp(s_i) v_i, O(S) = W(S)/Z(S); a shard returns
   (O, log Z); two shards merge by lerp / sigmoid / logaddexp; an empty shard is log Z = -inf
   and its vector is never read.

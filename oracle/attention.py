@@ -36,7 +36,7 @@ NEG_INF = -np.inf
 def shard_ranges(n: int, n_shards: int, page_size: int) -> list[tuple[int, int]]:
     """Position ranges [lo, hi) of the ``n_shards`` shards of a request with ``n`` cached positions.
 
-    §5 allows any split ("no split has to be balanced, contiguous or known in advance").  The
+    By §5 any partition of the positions merges to the same result, so the split is free.  The
     library fixes one, restated here from its description: the request's positions fill
     ceil(n / P) pages; every shard takes the next ceil(pages / S) pages (the last shards may get
     fewer pages, or none); the positions of the last page are clipped to n.

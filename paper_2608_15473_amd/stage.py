@@ -1,7 +1,7 @@
 """A stack of Q-First decoder blocks at one decode step, with the cache sweep on its own stream.
 
-Q-First (arXiv:2608.15473): in the rewired block the query reads the block input u while the key
-and value read the post-feed-forward stream z = u + M(N2 u) (§2); the block is
+Q-First (arXiv:2608.15473): in the rewired block the query is projected from the block input u,
+and the key and value from z = u + M(N2 u), the stream after the feed-forward (§2); the block is
 (I + A_{x;z}) o (I + M) (§8), so its output is y = z + W_o attn.  The sweep needs the query alone
 (§2), and neither it nor the feed-forward is downstream of the other (§3, "across layers"), so
 the two may run at once.  On one GPU this module offers three orders of the same launches:
