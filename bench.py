@@ -94,6 +94,68 @@ def kernel_source_digest():
     return h.hexdigest()
 
 
+def cpu_model():
+    """The host CPU's model name (what lscpu reports), from /proc/cpuinfo."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def env_info():
+    """Where and on what a result was measured: git commit (when the tree has git metadata, else
+    QF_GIT_SHA from the environment), source digest, ROCm / HIP / torch versions, GPU, host CPU
+    model and the cores this process may use."""
+    import subprocess
+
+    import torch
+
+    sha = None
+    try:
+        r = subprocess.run(["git", "rev-parse", "HEAD"], cwd=ROOT, capture_output=True, text=True,
+                           timeout=10)
+        sha = r.stdout.strip() or None
+    except (OSError, subprocess.SubprocessError):
+        pass
+    rocm = None
+    try:
+        with open(os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), ".info", "version")) as f:
+            rocm = f.read().strip()
+    except OSError:
+        pass
+    props = torch.cuda.get_device_properties(0)
+    import platform
+
+    from paper_2608_15473_amd.report import source_digest
+
+    return {"git_sha": sha or os.environ.get("QF_GIT_SHA"), "source_sha256": source_digest(),
+            "rocm": rocm, "hip": torch.version.hip, "torch": torch.__version__,
+            "gpu": props.name, "gpu_arch": getattr(props, "gcnArchName", None),
+            "gpu_compute_units": props.multi_processor_count, "cpu_model": cpu_model(),
+            "host_cores": len(os.sched_getaffinity(0)), "host": platform.node(),
+            "time": int(time.time())}
+
+
+def write_record(path, result):
+    """Append one result line to the run record of its workload (a JSON file holding a list of
+    runs), creating it if needed."""
+    runs = []
+    if os.path.exists(path):
+        with open(path) as f:
+            runs = json.load(f)["runs"]
+    runs.append(result)
+    d = os.path.dirname(path)
+    if d:
+        os.makedirs(d, exist_ok=True)
+    with open(path, "w") as f:
+        json.dump({"workload": result["config"]["workload"], "runs": runs}, f, indent=1)
+        f.write("\n")
+
+
 def cpu_baseline(cases, budget_s=15.0):
     """The fp64 oracle (sweep per shard + pairwise merge) timed on the host over a bounded sample:
     whole requests, layer after layer, added until about ``budget_s`` of CPU work.  Device-to-host
@@ -136,7 +198,8 @@ def cpu_baseline(cases, budget_s=15.0):
             break
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     return {"value": done_bytes / max(spent, 1e-9) / 1e9, "unit": "GB/s", "cores": int(threads),
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu_model(),
+            "host_cores": len(os.sched_getaffinity(0)),
             "sample": f"{reqs} whole request(s) from the first {layers} layer(s) in {passes} "
                       f"pass(es) "
                       f"({done_bytes / 1e6:.0f} MB of KV, all "
@@ -232,6 +295,9 @@ def run_stage(args, dev):
     if not args.no_cpu_baseline:
         log("[stage] cpu_baseline: timing the fp64 block oracle on a bounded sample")
         result["cpu_baseline"] = stage_cpu_baseline(stack, u, w, shape)
+    result["env"] = env_info()
+    if args.record:
+        write_record(args.record, result)
     print(json.dumps(result), flush=True)
 
 
@@ -320,7 +386,8 @@ def stage_cpu_baseline(stack, u, w, shape, budget_s=10.0):
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     steps = blocks / len(stack.layers)
     return {"value": round(w.batch * steps / spent, 4), "unit": "tokens/s", "cores": int(threads),
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu_model(),
+            "host_cores": len(os.sched_getaffinity(0)),
             "sample": f"{blocks} block(s) of the stack at context {w.ctx} (fp64 numpy, q/k/v, "
                       f"feed-forward and attention over the cache plus the current token), "
                       f"{spent:.1f} s; host has {len(os.sched_getaffinity(0))} usable cores"}
@@ -343,6 +410,8 @@ def main():
                          "launches dominate (small steps)")
     ap.add_argument("--stage", default=None,
                     help="time the [MLP || Attn] decode stage of this block workload instead")
+    ap.add_argument("--record", default=None,
+                    help="also append the result line to this run-record file (JSON)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="instead of the bench: one plain device copy of this many MiB (the "
                          "known-size reference that scales the FETCH_SIZE / WRITE_SIZE counters)")
@@ -491,6 +560,9 @@ def main():
     if not args.no_cpu_baseline:
         log("[bench] cpu_baseline: timing the fp64 oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(cases[:L])
+    result["env"] = env_info()
+    if args.record:
+        write_record(args.record, result)
     print(json.dumps(result), flush=True)
 
 
