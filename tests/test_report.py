@@ -35,8 +35,9 @@ def test_records_are_complete_and_consistent(fname, workload, run):
     if "kernels" in run:        # a decode-stage record
         return
     # value = KV bytes per step / step time; the roofline fraction = achieved / peak
-    v = run["config"]["kv_bytes_per_step"] / (run["ms_per_step"] / 1e3) / 1e9
-    assert abs(v - run["value"]) <= 1e-3 * v
+    ms = run["ms_per_step"]
+    v = run["config"]["kv_bytes_per_step"] / (ms / 1e3) / 1e9
+    assert abs(v - run["value"]) <= v * (1e-3 + 0.5e-4 / ms)     # ms printed to 4 decimals
     roof = run["roofline"]
     assert abs(roof["achieved"] / roof["peak"] - roof["frac"]) <= 1e-3
     ach = roof["algorithmic_bytes"] / (roof["launch_avg_us"] / 1e6) / 1e9
