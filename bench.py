@@ -472,54 +472,71 @@ def main():
     turn = [0]
     # The two-launch step of each resident copy, checked and converted once (the host then does
     # two foreign calls per layer; the small single-layer workload is otherwise host-bound).
+    # Every launch goes to one stream of our own (default priority): the legacy null stream
+    # synchronises implicitly with other streams, which costs launch-bound steps a few percent.
+    run_stream = torch.cuda.Stream(dev)
     plans = [] if args.one_launch else [
         qf.DecodeStepPlan(c.q, c.k_cache, c.v_cache, c.block_table, c.ctx_lens, c.n_shards,
                           max_shards=S, scale=c.scale, part_out=po, part_lse=pl, out=out, lse=lse,
-                          fold_chunks=False) for c in cases]
+                          fold_chunks=False, stream=run_stream.cuda_stream) for c in cases]
+    torch.cuda.synchronize()
+
+    # The sweep's launch duration is timed with HIP events on a sample of the timed region's
+    # launches: every EVERY-th sweep (one layer per step for a model of 8+ layers, every 8th step
+    # otherwise).  Events around every launch would add their host cost to each step, which on the
+    # launch-bound workloads (one small layer, the per-GPU share) is most of a step's host time.
+    EVERY = L if L >= 8 else 8
+    launches = [0]
 
     def step(events=None):
         base = turn[0]
         turn[0] += L
         for l in range(L):
             c = cases[(base + l) % copies]
-            if events is not None:
-                events[l][0].record()
+            timed = events is not None and launches[0] % EVERY == 0
+            launches[0] += 1
+            if timed:
+                pair = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                events.append(pair)
+                pair[0].record()
             if not args.one_launch:
                 plans[(base + l) % copies].split()
             else:
                 qf.attn_decode(c.q, c.k_cache, c.v_cache, c.block_table, c.ctx_lens,
                                c.n_shards, max_shards=S, scale=c.scale, out=out, lse=lse,
                                workspace=ws, counters=counters)
-            if events is not None:
-                events[l][1].record()
+            if timed:
+                pair[1].record()
             if not args.one_launch:
                 plans[(base + l) % copies].combine()
 
-    warm, t_w = 0, time.perf_counter()
-    while (warm < args.warmup) if args.warmup is not None else \
-            (warm < 3 or time.perf_counter() - t_w < WARMUP_SECONDS):
-        step()
-        warm += 1
-        if args.warmup is None:
-            torch.cuda.synchronize()
-    torch.cuda.synchronize()
-    per_step = (time.perf_counter() - t_w) / max(1, warm)
-    if args.steps is None:
-        args.steps = max(10, int(TIMED_SECONDS / max(per_step, 1e-6)) + 1)
-    args.warmup = warm
-    log(f"[bench] warmup done ({warm} steps); timing {args.steps} steps")
-    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(L)]
-          for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for k in range(args.steps):
-        step(ev[k])
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t_start
+    with torch.cuda.stream(run_stream):
+        warm, t_w = 0, time.perf_counter()
+        while (warm < args.warmup) if args.warmup is not None else \
+                (warm < 3 or time.perf_counter() - t_w < WARMUP_SECONDS):
+            step()
+            warm += 1
+            if args.warmup is None:
+                torch.cuda.synchronize()
+        torch.cuda.synchronize()
+        per_step = (time.perf_counter() - t_w) / max(1, warm)
+        if args.steps is None:
+            args.steps = max(10, int(TIMED_SECONDS / max(per_step, 1e-6)) + 1)
+        args.warmup = warm
+        log(f"[bench] warmup done ({warm} steps); timing {args.steps} steps")
+        ev = []
+        launches[0] = 0
+        torch.cuda.synchronize()
+        t_start = time.perf_counter()
+        for k in range(args.steps):
+            step(ev)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t_start
     ms_per_step = elapsed * 1e3 / args.steps
-    sweep_ms = [ev[k][l][0].elapsed_time(ev[k][l][1]) for k in range(args.steps) for l in range(L)]
+    sweep_ms = [a.elapsed_time(b) for a, b in ev]
     sweep_avg_s = sum(sweep_ms) / len(sweep_ms) / 1e3
-    log(f"[bench] {ms_per_step:.3f} ms/step, sweep launch avg {sweep_avg_s * 1e6:.1f} us")
+    log(f"[bench] {ms_per_step:.3f} ms/step, sweep launch avg {sweep_avg_s * 1e6:.1f} us "
+        f"({len(sweep_ms)} timed launches)")
 
     ab = ab[:L]                     # every copy has the same lengths, so the same bytes
     kv_step = sum(a["kv"] for a in ab)
@@ -553,6 +570,7 @@ def main():
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "kernel": "decode_fused_kernel" if args.one_launch else "decode_split_kernel",
                      "launch_avg_us": round(sweep_avg_s * 1e6, 2),
+                     "timed_launches": len(sweep_ms),
                      "algorithmic_bytes": int(sweep_bytes),
                      "traffic": committed_traffic(w.name, not args.one_launch)
                      if L == w.layers else None},

@@ -160,10 +160,16 @@ __device__ __forceinline__ void sweep_unit(
   //  * Short shards (kOrderByRequest): each XCD takes a contiguous range of units in (request,
   //    shard, chunk, KV head) order, so a request's query, context length and block-table lines
   //    stay in one XCD's L2 and the short workgroups' prologues hit there.
-  //  * Long shards (kOrderByShardDesc): units in (shard descending, request, chunk, KV head) order,
+  //  * Long shards (kOrderByShardDesc): units in (shard descending, request, KV head) order,
   //    round-robin over the XCDs, so the largest shards (high indices exist only in long requests)
-  //    start first and every XCD gets an even share; the small shards fill the tail.
+  //    start first and every XCD gets an even share; the small shards fill the tail.  With
+  //    sub-shard chunks the chunk index runs fastest, so the chunks of a shard alternate between
+  //    even- and odd-numbered XCDs (the unit index modulo 8 is the XCD), and their sizes are
+  //    weighted by that parity (kXcdWeightEven / kXcdWeightOdd): measured on MI355X, odd-numbered
+  //    XCDs stream 8-17% slower than even ones under the long-shard sweep, whatever KV head they
+  //    read, so equal chunks leave the even XCDs idle while the odd ones finish.
   int g, c, s, b;
+  int pair = 0;  // long shards with chunks: index of the (request, shard, KV head) in unit order
   if (order == kOrderByRequest) {
     const int unit = (int)(bid % 8u) * units_per_xcd + (int)(bid / 8u);
     if (unit >= n_units) return;
@@ -176,10 +182,17 @@ __device__ __forceinline__ void sweep_unit(
   } else {
     const int unit = (int)bid;
     if (unit >= n_units) return;
-    g = unit % hkv;
-    int rest = unit / hkv;
-    c = rest % chunks;
-    rest /= chunks;
+    int rest;
+    if (chunks > 1) {
+      c = unit % chunks;
+      pair = unit / chunks;
+      g = pair % hkv;
+      rest = pair / hkv;
+    } else {
+      c = 0;
+      g = unit % hkv;
+      rest = unit / hkv;
+    }
     b = rest % batch;
     s = max_shards - 1 - rest / batch;
   }
@@ -200,9 +213,23 @@ __device__ __forceinline__ void sweep_unit(
     p1 = (int)min((int64_t)(s + 1) * per, (int64_t)pages);
   }
   const int len = p1 - p0;
-  const int cper = (len + chunks - 1) / chunks;
-  const int c0 = p0 + (int)min((int64_t)c * cper, (int64_t)len);
-  const int c1 = p0 + (int)min((int64_t)(c + 1) * cper, (int64_t)len);
+  int c0, c1;
+  if (order == kOrderByShardDesc && chunks > 1) {
+    // Chunk j of this shard runs on an XCD of parity (pair * chunks + j) % 2; the pages before
+    // chunk c weigh kXcdWeightEven per even-XCD chunk and kXcdWeightOdd per odd one.
+    const int first_odd = (int)(((int64_t)pair * chunks) & 1);
+    auto weight_before = [&](int cc) -> int64_t {
+      const int64_t even = first_odd ? cc / 2 : (cc + 1) / 2;
+      return even * kXcdWeightEven + (cc - even) * kXcdWeightOdd;
+    };
+    const int64_t total = weight_before(chunks);
+    c0 = p0 + (int)((int64_t)len * weight_before(c) / total);
+    c1 = p0 + (int)((int64_t)len * weight_before(c + 1) / total);
+  } else {
+    const int cper = (len + chunks - 1) / chunks;
+    c0 = p0 + (int)min((int64_t)c * cper, (int64_t)len);
+    c1 = p0 + (int)min((int64_t)(c + 1) * cper, (int64_t)len);
+  }
 
   // An empty unit (a slot past the request's shards, or an empty shard or chunk) reads nothing:
   // its ln Z is -inf (NaN if the request's shape was out of range), its O is never read, so it

@@ -25,6 +25,10 @@ constexpr int kOrderByRequest = 0;
 constexpr int kOrderByShardDesc = 1;
 // Shards at least this long (pages, at full capacity) are swept in kOrderByShardDesc.
 constexpr int kLongShardPages = 128;
+// Relative page shares of the sub-shard chunks of a long shard that run on even- and odd-numbered
+// XCDs (decode_split.hip): the odd XCDs stream slower.
+constexpr int kXcdWeightEven = 1080;
+constexpr int kXcdWeightOdd = 920;
 
 // One launch of the sweep kernel.  A workgroup handles one unit (request b, shard s, chunk c,
 // KV head g); its output slot is [((b * max_shards + s) * chunks + c) * hq + g * G + h].
