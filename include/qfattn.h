@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define QF_VERSION 6
+#define QF_VERSION 7
 
 #define QF_OK 0
 #define QF_EINVAL (-1)       /* null pointer, negative or inconsistent size, Hq % Hkv != 0   */
@@ -71,7 +71,12 @@ typedef struct qf_decode_desc {
 /*
  * Bytes of device workspace qf_attn_decode_split needs for this shape (0 is possible).  The
  * workspace holds partial states of sub-shard chunks when a shape has fewer (request, KV head,
- * shard) units than the sweep keeps resident on the GPU at once.  Host call; depends on the
+ * shard) units than the sweep keeps resident on the GPU at once, and, for a batch of several
+ * requests whose shards (sub-shard chunks, if any) are long, 128+ pages each at full capacity
+ * (ceil(max_pages_per_seq / max_shards) / C >= 128), the sweep's dispatch order:
+ * B * max_shards int32, the (request, shard) pairs ranked by length, longest first, by a small
+ * kernel enqueued just before the sweep (the order decides only when each shard is swept, never
+ * the results, which are the same bits in any order).  Host call; depends on the
  * descriptor and on that resident count, which is queried from the current device once per
  * process (an MI355X is assumed when there is no device), so query and launch agree.
  * Returns QF_OK, or QF_EINVAL / QF_EUNSUPPORTED for a descriptor qf_attn_decode_split rejects.
@@ -130,7 +135,9 @@ int qf_attn_decode_split_chunks(const qf_decode_desc* desc, int32_t* chunks);
  * qf_attn_decode_split).  A chunk is itself a shard of a finer split of the same cache (§5: any
  * partition), so qf_attn_combine over the max_shards * C slots gives the result of the folded
  * sweep followed by the combine, up to the order of the fp32 sums, with one launch fewer and no
- * workspace: for callers that need only the merged attention, not per-shard partials.
+ * workspace: for callers that need only the merged attention, not per-shard partials.  Having no
+ * workspace, it sweeps long shards in their plain order (shard index descending, never ranked
+ * by length); with C == 1 qf_attn_decode_split is the faster call on a ragged batch.
  *
  *   q ... n_shards   as for qf_attn_decode_split.
  *   slot_out    fp32 [B, n_slots, Hq, D], 16-byte aligned: O of every non-empty chunk.
@@ -150,11 +157,12 @@ int qf_attn_decode_split_unfolded(const qf_decode_desc* desc, const void* q, con
  * The sweep and the merge in ONE launch: the result of qf_attn_decode_split followed by
  * qf_attn_combine on the same inputs, without materialising the per-shard outputs in caller
  * buffers.  Bitwise the same when the shape needs no sub-shard chunks
- * (qf_attn_decode_split_workspace_size() == 0) and max_shards <= 64; otherwise the slots are
+ * (qf_attn_decode_split_chunks() == 1) and max_shards <= 64; otherwise the slots are
  * grouped differently (the chunks of every shard merge in the same pass as the shards; more than
- * 64 slots are summed by 4 wavefronts instead of 16), which can move the last bits.  The last workgroup to finish a (request, KV head) merges that group's slots
- * (partial states stay in the workspace), so the merge's launch and its wait for the sweep's
- * tail disappear.
+ * 64 slots are summed by 4 wavefronts instead of 16), which can move the last bits.  The last
+ * workgroup to finish a (request, KV head) merges that group's slots (partial states stay in the
+ * workspace), so the merge's launch and its wait for the sweep's tail disappear.  Being one
+ * launch, it sweeps long shards in their plain order (no ranking by length).
  *
  *   q ... n_shards   as for qf_attn_decode_split.
  *   out              bf16 [B, Hq, D], 4-byte aligned; lse fp32 [B, Hq] natural log, or NULL.
@@ -363,7 +371,8 @@ typedef struct {
  * The sweep beside the feed-forward (§3, "across layers": neither is downstream of the other, so
  * they may run at once): exactly qf_attn_decode_split(desc, q, ..., workspace_size) and
  * qf_linear(*beside), issued as ONE launch whose workgroups take either role, so that on one GPU
- * the two share every CU instead of running one after the other.  Results are bitwise those of
+ * the two share every CU instead of running one after the other (preceded by the ranking kernel
+ * where qf_attn_decode_split ranks the shape's shards).  Results are bitwise those of
  * the two separate calls.  The caller guarantees that neither call's outputs overlap the other's
  * inputs or outputs.  Arguments, errors and ownership are those of the two calls (checked before
  * anything is launched); `beside` is a HOST pointer, read during the call.  With batch == 0 or

@@ -270,9 +270,11 @@ class DecodeStepPlan:
 
     The arguments are those of ``attn_decode_split`` (plus ``out`` / ``lse`` of ``attn_combine``);
     every tensor, the workspace included, is allocated here when not given and kept by the plan.
-    With ``fold_chunks=False`` the sweep is ``attn_decode_split_unfolded`` (its sub-shard chunks
-    stay slots of part_out / part_lse, [B, S_max * C, ...], and the combine merges them: one launch
-    fewer when the shape is chunked); otherwise part_out / part_lse are the per-shard partials.
+    With ``fold_chunks=False`` and a chunked shape the sweep is ``attn_decode_split_unfolded`` (its
+    sub-shard chunks stay slots of part_out / part_lse, [B, S_max * C, ...], and the combine merges
+    them: one launch fewer); otherwise, C == 1 included, it is ``attn_decode_split`` and part_out /
+    part_lse are the per-shard partials (with C == 1 the two calls give the same bits, and the
+    split, having a workspace, also ranks a ragged batch's long shards by length).
     Calling the plan enqueues the two library calls on ``stream`` (default: the current stream at
     construction) with the pointers taken at construction, so the caller updates tensors in
     place (e.g. the query, the cache, ctx_lens) and never reallocates them; per call the host does
@@ -286,6 +288,11 @@ class DecodeStepPlan:
         args, desc, part_out, part_lse, workspace, n_shards = _split_call(
             q, k_cache, v_cache, block_table, ctx_lens, n_shards, max_shards, scale, part_out,
             part_lse, workspace, max_pages, unfolded=not fold_chunks)
+        if not fold_chunks and split_chunks(desc) == 1:
+            fold_chunks = True
+            args, desc, part_out, part_lse, workspace, n_shards = _split_call(
+                q, k_cache, v_cache, block_table, ctx_lens, n_shards, desc.max_shards,
+                desc.softmax_scale, part_out, part_lse, workspace, max_pages)
         B, S, Hq, D = part_out.shape
         if out is None:
             out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=q.device)

@@ -29,6 +29,9 @@ constexpr int kLongShardPages = 128;
 // XCDs (decode_split.hip): the odd XCDs stream slower.
 constexpr int kXcdWeightEven = 1080;
 constexpr int kXcdWeightOdd = 920;
+// Length buckets (and threads) of the one-workgroup kernel that ranks the shards of a long-shard
+// sweep over several requests by length (decode_split.hip).
+constexpr int kRankBuckets = 1024;
 
 // One launch of the sweep kernel.  A workgroup handles one unit (request b, shard s, chunk c,
 // KV head g); its output slot is [((b * max_shards + s) * chunks + c) * hq + g * G + h].
@@ -45,6 +48,11 @@ struct SplitParams {
   int32_t n_units;              // B * max_shards * chunks * Hkv
   int32_t units_per_xcd;        // ceil(n_units / 8)
   int32_t order;                // kOrderByRequest or kOrderByShardDesc (dispatch order of units)
+  // kOrderByShardDesc only, or null: [B * max_shards] int32 that a ranking kernel, launched just
+  // before the sweep, fills with the (shard, request) pairs in dispatch order, longest shard first
+  // (rank_shift: log2 of the length buckets' width in pages).
+  int32_t* pair_order;
+  int32_t rank_shift;
   bool deep;                    // short shards of >= kDeepMinPages pages: split_buffers_deep(G)
   float scale_log2;             // softmax scale * log2(e)
 };

@@ -74,10 +74,29 @@ int64_t choose_chunks(const qf_decode_desc* d) {
   return std::max<int64_t>(1, std::min<int64_t>(c, 1024));
 }
 
-size_t workspace_bytes(const qf_decode_desc* d, int64_t chunks) {
+// Long shards: long-lived workgroups, the dispatch order decides the tail (largest first).
+// Short shards: short workgroups, prologue latency decides (keep a request on one XCD).
+int sweep_order(const qf_decode_desc* d, int64_t chunks) {
+  const int64_t shard_pages = (d->max_pages_per_seq + d->max_shards - 1) / d->max_shards / chunks;
+  return shard_pages >= qf::kLongShardPages ? qf::kOrderByShardDesc : qf::kOrderByRequest;
+}
+
+// A long-shard sweep over several requests ranks its (shard, request) pairs by length before it
+// starts (one int32 per pair of workspace); one request's shards are all of one length already.
+bool ranks_shards(const qf_decode_desc* d, int64_t chunks) {
+  return d->batch > 1 && sweep_order(d, chunks) == qf::kOrderByShardDesc;
+}
+
+size_t chunk_state_bytes(const qf_decode_desc* d, int64_t chunks) {
   if (chunks <= 1) return 0;
   const size_t states = (size_t)d->batch * d->max_shards * chunks * d->n_q_heads;
   return states * qf::kHeadDim * sizeof(float) + states * sizeof(float);
+}
+
+// qf_attn_decode_split's workspace: the chunk states, then the pair order.
+size_t workspace_bytes(const qf_decode_desc* d, int64_t chunks) {
+  const size_t order = ranks_shards(d, chunks) ? (size_t)d->batch * d->max_shards * sizeof(int32_t) : 0;
+  return chunk_state_bytes(d, chunks) + order;
 }
 
 // Everything qf_attn_decode_split checks and derives before launching.
@@ -90,10 +109,13 @@ struct Split {
   qf::MergeParams chunk_merge{};
 };
 
+// fold: the chunks are folded into part_out / part_lse (chunk states in the workspace) or left
+// as slots there; rank: the workspace also holds the pair order of a ranked sweep.  The workspace
+// is needed for whichever of the two applies.
 int prepare_split(const qf_decode_desc* desc, const void* q, const void* k_cache,
                   const void* v_cache, const int32_t* block_table, const int32_t* ctx_lens,
                   const int32_t* n_shards, float* part_out, float* part_lse, void* workspace,
-                  size_t workspace_size, Split* sp, bool fold = true) {
+                  size_t workspace_size, Split* sp, bool fold = true, bool rank = true) {
   int rc = check_desc(desc);
   if (rc) return rc;
   const qf_decode_desc& d = *desc;
@@ -113,7 +135,9 @@ int prepare_split(const qf_decode_desc* desc, const void* q, const void* k_cache
                 (long long)d.batch * d.max_pages_per_seq, d.num_pages);
 
   const int64_t chunks = choose_chunks(&d);
-  const size_t need = fold ? workspace_bytes(&d, chunks) : 0;
+  const size_t state_bytes = fold ? chunk_state_bytes(&d, chunks) : 0;
+  rank = rank && ranks_shards(&d, chunks);
+  const size_t need = state_bytes + (rank ? (size_t)d.batch * d.max_shards * sizeof(int32_t) : 0);
   if (need) {
     if (!workspace) return fail(QF_EINVAL, "this shape needs %zu bytes of workspace", need);
     if (workspace_size < need)
@@ -147,10 +171,12 @@ int prepare_split(const qf_decode_desc* desc, const void* q, const void* k_cache
   p.chunks = (int32_t)chunks;
   p.n_units = (int32_t)units;
   p.units_per_xcd = (int32_t)((units + 7) / 8);
-  // Long shards: long-lived workgroups, the dispatch order decides the tail (largest first).
-  // Short shards: short workgroups, prologue latency decides (keep a request on one XCD).
   const int64_t shard_pages = (d.max_pages_per_seq + d.max_shards - 1) / d.max_shards / chunks;
-  p.order = shard_pages >= qf::kLongShardPages ? qf::kOrderByShardDesc : qf::kOrderByRequest;
+  p.order = sweep_order(&d, chunks);
+  p.pair_order = rank ? reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + state_bytes)
+                      : nullptr;
+  p.rank_shift = 0;
+  while ((d.max_pages_per_seq >> p.rank_shift) >= qf::kRankBuckets) ++p.rank_shift;
   // Deep buffers cost occupancy (two wavefronts per SIMD instead of three), so a chunked sweep,
   // whose chunk count fills exactly the resident workgroups of the two-buffer kernel, keeps two
   // buffers (deep ones would leave a second, partial round: -2% on the 131,072-position share).
@@ -309,7 +335,7 @@ int qf_attn_decode_split_unfolded(const qf_decode_desc* desc, const void* q, con
                 n_slots, (long long)want);
   Split sp;
   rc = prepare_split(desc, q, k_cache, v_cache, block_table, ctx_lens, n_shards, slot_out,
-                     slot_lse, nullptr, 0, &sp, false);
+                     slot_lse, nullptr, 0, &sp, false, false);
   if (rc || sp.noop) return rc;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const hipError_t e = qf::launch_decode_split(sp.p, sp.group, s);
@@ -396,7 +422,7 @@ int decode_fused(const qf_decode_desc* desc, const void* q, const void* k_cache,
   Split sp;
   rc = prepare_split(desc, q, k_cache, v_cache, block_table, ctx_lens, n_shards, states,
                      states + n_states * qf::kHeadDim, chunks > 1 ? workspace : nullptr,
-                     chunks > 1 ? need : 0, &sp);
+                     chunks > 1 ? need : 0, &sp, true, false);
   if (rc || sp.noop) return rc;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (fixed_scratch) {

@@ -81,12 +81,24 @@ def test_bad_descriptor_is_rejected(kw, code):
     assert rc2 == code
 
 
-def test_workspace_only_when_units_are_few():
+def _order_bytes(d, chunks):
+    """The header's rule for the dispatch order in the workspace: a batch of several requests
+    whose shards (or chunks) are 128+ pages long at full capacity ranks its B * S_max pairs."""
+    long = -(-d.max_pages_per_seq // d.max_shards) // chunks >= 128
+    return 4 * d.batch * d.max_shards if d.batch > 1 and long else 0
+
+
+def test_workspace_only_when_units_are_few_or_shards_are_ranked():
     rc, n = _ws(_desc(batch=32, max_shards=64, max_pages_per_seq=2048, num_pages=65536))
-    assert rc == 0 and n == 0
+    assert rc == 0 and n == 0                              # short shards, many units
     rc, n = _ws(_desc(batch=1, max_shards=16, max_pages_per_seq=65536, num_pages=65536))
-    assert rc == 0 and n > 0
+    assert rc == 0 and n > 0                               # chunk states
     assert n % 16 == 0
+    rc, n = _ws(_desc(batch=48, max_shards=16, max_pages_per_seq=2560, num_pages=65536))
+    assert rc == 0 and n == 48 * 16 * 4                    # 160-page shards: the order only
+    rc, n = _ws(_desc(batch=64, n_q_heads=32, max_shards=32, max_pages_per_seq=8192,
+                      num_pages=140000))
+    assert rc == 0 and n == 64 * 32 * 4                    # the ragged 64-request batch
 
 
 def _chunks(**kw):
@@ -94,8 +106,10 @@ def _chunks(**kw):
     rc, n = _ws(d)
     assert rc == 0
     per_chunk = d.batch * d.max_shards * d.n_q_heads * (128 + 1) * 4
-    assert n % per_chunk == 0
-    return n // per_chunk
+    for c in range(0, 2049):                               # n = chunk states + dispatch order
+        if n == c * per_chunk + _order_bytes(d, max(c, 1)):
+            return c
+    raise AssertionError(f"workspace of {n} bytes fits no chunk count")
 
 
 # Sweep workgroups resident on one MI355X (256 CUs) per group size: what the library assumes
@@ -304,8 +318,9 @@ def test_binding_refuses_cpu_tensors():
 
 
 def test_chunk_count_agrees_with_the_workspace():
-    """qf_attn_decode_split_chunks gives the chunk count behind the workspace size: C > 1 exactly
-    when a workspace is needed, whose size is then B * S * C * Hq * (128 + 1) fp32."""
+    """qf_attn_decode_split_chunks gives the chunk count behind the workspace size: the chunk
+    states are B * S * C * Hq * (128 + 1) fp32 when C > 1 (none when C == 1), followed by the
+    dispatch order of a ranked shape (B * S int32)."""
     lib = load_library()
     for kw in [dict(batch=1, max_shards=16, max_pages_per_seq=65536, num_pages=65536),
                dict(batch=1, max_shards=8, max_pages_per_seq=288, num_pages=288),
@@ -319,7 +334,8 @@ def test_chunk_count_agrees_with_the_workspace():
         rc, n = _ws(d)
         assert rc == 0 and c.value >= 1
         per_chunk = d.batch * d.max_shards * d.n_q_heads * (128 + 1) * 4
-        assert n == (0 if c.value == 1 else c.value * per_chunk), (kw, c.value, n)
+        states = 0 if c.value == 1 else c.value * per_chunk
+        assert n == states + _order_bytes(d, c.value), (kw, c.value, n)
     bad = _desc(n_q_heads=12, n_kv_heads=8)
     assert lib.qf_attn_decode_split_chunks(ctypes.byref(bad), ctypes.byref(c)) == qf.QF_EINVAL
     assert lib.qf_attn_decode_split_chunks(ctypes.byref(_desc()), None) == qf.QF_EINVAL

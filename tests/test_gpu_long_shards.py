@@ -1,11 +1,13 @@
 """GPU parity of ragged batches with long shards against the fp64 oracle.
 
 Shapes with many (request, shard, KV head) units whose shards are long (128+ pages per shard at full
-capacity) are swept largest shard first, one workgroup per unit.  Every output of every case is
-checked: per-shard partials and the combined result, at every group size, including requests with
-no positions, partial last pages, more shards than pages, very little work in all, one long request
-next to many short ones, out-of-range device values, and the unfolded sweep (chunks left as slots)
-followed by the combine."""
+capacity) are swept longest shard first, one workgroup per unit: the split sweep ranks the
+(request, shard) pairs by length in its workspace before it starts, the unfolded sweep (no
+workspace) takes them by shard index, descending.  Every output of every case is checked:
+per-shard partials and the combined result, at every group size, including requests with no
+positions, partial last pages, more shards than pages, very little work in all, one long request
+next to many short ones, out-of-range device values, the unfolded sweep followed by the combine
+(bitwise the ranked sweep's result), and the sweep sharing its launch with a product."""
 
 import numpy as np
 import pytest
@@ -24,10 +26,13 @@ def _desc(case):
 
 def _is_long_shard_shape(case):
     """128+ pages per shard at full capacity and at least one full set of resident workgroups'
-    worth of units (no sub-shard chunks)."""
+    worth of units (no sub-shard chunks); the split sweep then ranks the B * S_max (request,
+    shard) pairs, and its workspace is that order."""
     B, S = case.q.shape[0], case.max_shards
     long = -(-case.block_table.shape[1] // S) >= 128
-    return long and qf.split_chunks(_desc(case)) == 1
+    desc = _desc(case)
+    ranked = qf.workspace_size(desc) == 4 * B * S
+    return long and qf.split_chunks(desc) == 1 and ranked
 
 
 def _ragged(batch, seed, n_max=40000):
@@ -122,3 +127,36 @@ def test_long_shards_are_deterministic(gpu):
     a, b = run_gpu(case), run_gpu(case)
     for key in ("part_out", "part_lse", "out_bits", "lse"):
         assert np.array_equal(a[key], b[key], equal_nan=True), key
+
+
+def test_long_shards_beside_a_product_equal_the_two_calls_bitwise(gpu):
+    """The sweep sharing one launch with a product (qf_attn_decode_split_beside, which ranks the
+    shards like the split sweep) gives bitwise the split sweep's and the product's outputs."""
+    n, S = _ragged(48, 460)
+    case = make_case(48, 4, 2, n, S, seed=460, max_shards=16, max_pages=2560, device=gpu)
+    assert _is_long_shard_shape(case)
+    args = (case.q, case.k_cache, case.v_cache, case.block_table, case.ctx_lens, case.n_shards)
+    gen = torch.Generator(device=gpu).manual_seed(461)
+    M, N, K = 2, 1024, 1024
+    x = torch.randn(M, K, generator=gen, device=gpu).to(torch.bfloat16)
+    w = (torch.randn(N, K, generator=gen, device=gpu) / K ** 0.5).to(torch.bfloat16)
+    g = (torch.rand(K, generator=gen, device=gpu) + 0.5).to(torch.bfloat16)
+    outs = []
+    for together in (False, True):
+        po = torch.full((48, 16, 4, 128), float("nan"), device=gpu)
+        pl = torch.full((48, 16, 4), float("nan"), device=gpu)
+        y = torch.full((M, N), float("nan"), device=gpu).to(torch.bfloat16)
+        lin = dict(x=x, w=w, prologue="rms_norm", gain=g, out=y)
+        say(f"[long shards] beside, together={together}")
+        if together:
+            qf.attn_decode_split_beside(*args, lin, max_shards=16, scale=case.scale, part_out=po,
+                                        part_lse=pl)
+        else:
+            qf.attn_decode_split(*args, max_shards=16, scale=case.scale, part_out=po, part_lse=pl)
+            qf.linear(**lin)
+        torch.cuda.synchronize()
+        outs.append((po.view(torch.int32).clone(), pl.view(torch.int32).clone(),
+                     y.view(torch.int16).clone()))
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+    assert not torch.isnan(outs[1][1].view(torch.float32)).any()
