@@ -71,12 +71,13 @@ typedef struct qf_decode_desc {
 /*
  * Bytes of device workspace qf_attn_decode_split needs for this shape (0 is possible).  The
  * workspace holds partial states of sub-shard chunks when a shape has fewer (request, KV head,
- * shard) units than the sweep keeps resident on the GPU at once, and, for a batch of several
- * requests whose shards (sub-shard chunks, if any) are long, 128+ pages each at full capacity
- * (ceil(max_pages_per_seq / max_shards) / C >= 128), the sweep's dispatch order:
- * B * max_shards int32, the (request, shard) pairs ranked by length, longest first, by a small
- * kernel enqueued just before the sweep (the order decides only when each shard is swept, never
- * the results, which are the same bits in any order).  Host call; depends on the
+ * shard) units than the sweep keeps resident on the GPU at once; otherwise, when the shards are
+ * long, 128+ pages each at full capacity (ceil(max_pages_per_seq / max_shards) >= 128), and
+ * B * max_shards <= 8192, the sweep's dispatch order: ceil(B * max_shards * Hkv / 8) * 8 int32,
+ * written by a small kernel enqueued just before the sweep (the (request, shard) pairs ranked by
+ * length, longest first, their units dealt to the GPU's XCDs by their measured speeds).  The
+ * order decides only when and where each unit is swept, never the results, which are the same
+ * bits in any order.  Host call; depends on the
  * descriptor and on that resident count, which is queried from the current device once per
  * process (an MI355X is assumed when there is no device), so query and launch agree.
  * Returns QF_OK, or QF_EINVAL / QF_EUNSUPPORTED for a descriptor qf_attn_decode_split rejects.
@@ -137,7 +138,7 @@ int qf_attn_decode_split_chunks(const qf_decode_desc* desc, int32_t* chunks);
  * sweep followed by the combine, up to the order of the fp32 sums, with one launch fewer and no
  * workspace: for callers that need only the merged attention, not per-shard partials.  Having no
  * workspace, it sweeps long shards in their plain order (shard index descending, never ranked
- * by length); with C == 1 qf_attn_decode_split is the faster call on a ragged batch.
+ * by length); with C == 1 qf_attn_decode_split is the faster call on long shards.
  *
  *   q ... n_shards   as for qf_attn_decode_split.
  *   slot_out    fp32 [B, n_slots, Hq, D], 16-byte aligned: O of every non-empty chunk.
@@ -162,7 +163,7 @@ int qf_attn_decode_split_unfolded(const qf_decode_desc* desc, const void* q, con
  * 64 slots are summed by 4 wavefronts instead of 16), which can move the last bits.  The last
  * workgroup to finish a (request, KV head) merges that group's slots (partial states stay in the
  * workspace), so the merge's launch and its wait for the sweep's tail disappear.  Being one
- * launch, it sweeps long shards in their plain order (no ranking by length).
+ * launch, it sweeps long shards in their plain order (no ranked dispatch order).
  *
  *   q ... n_shards   as for qf_attn_decode_split.
  *   out              bf16 [B, Hq, D], 4-byte aligned; lse fp32 [B, Hq] natural log, or NULL.

@@ -183,7 +183,7 @@ __device__ __forceinline__ void sweep_unit(
     int32_t max_pages, int32_t num_pages, int32_t max_shards, int32_t chunks, int32_t n_units,
     int32_t units_per_xcd, int32_t batch, int32_t order, float scale_log2, const unsigned bid,
     int32_t* __restrict__ counters = nullptr, uint16_t* __restrict__ merged_o = nullptr,
-    float* __restrict__ merged_lse = nullptr, const int32_t* __restrict__ pair_order = nullptr) {
+    float* __restrict__ merged_lse = nullptr, const int32_t* __restrict__ unit_order = nullptr) {
   // Which unit this workgroup sweeps.  Workgroups are dispatched in index order, round-robin over
   // the 8 XCDs.
   //  * Short shards (kOrderByRequest): each XCD takes a contiguous range of units in (request,
@@ -197,8 +197,8 @@ __device__ __forceinline__ void sweep_unit(
   //    weighted by that parity (kXcdWeightEven / kXcdWeightOdd): measured on MI355X, odd-numbered
   //    XCDs stream 8-17% slower than even ones under the long-shard sweep, whatever KV head they
   //    read, so equal chunks leave the even XCDs idle while the odd ones finish.
-  //    With a pair order (a batch of several requests) the (shard, request) pairs are taken in
-  //    the ranked order instead: longest shard first, whatever its request and index.
+  //    Without chunks, a unit order (rank_units_kernel) replaces both: each workgroup index
+  //    names its unit, longest shard first, and the odd XCDs get fewer of the long units.
   int g, c, s, b;
   int pair = 0;  // long shards with chunks: index of the (request, shard, KV head) in unit order
   if (order == kOrderByRequest) {
@@ -211,8 +211,8 @@ __device__ __forceinline__ void sweep_unit(
     s = rest % max_shards;
     b = rest / max_shards;
   } else {
-    const int unit = (int)bid;
-    if (unit >= n_units) return;
+    const int unit = unit_order != nullptr ? unit_order[bid] : (int)bid;
+    if (unit < 0 || unit >= n_units) return;
     int rest;
     if (chunks > 1) {
       c = unit % chunks;
@@ -224,7 +224,6 @@ __device__ __forceinline__ void sweep_unit(
       g = unit % hkv;
       rest = unit / hkv;
     }
-    if (pair_order != nullptr) rest = pair_order[rest];
     b = rest % batch;
     s = max_shards - 1 - rest / batch;
   }
@@ -609,40 +608,114 @@ decode_split_kernel(const uint16_t* __restrict__ qp, const uint16_t* __restrict_
                     float* __restrict__ out_o, float* __restrict__ out_lse, int32_t hq,
                     int32_t hkv, int32_t max_pages, int32_t num_pages, int32_t max_shards,
                     int32_t chunks, int32_t n_units, int32_t units_per_xcd, int32_t batch,
-                    int32_t order, float scale_log2, const int32_t* __restrict__ pair_order) {
+                    int32_t order, float scale_log2, const int32_t* __restrict__ unit_order) {
   sweep_unit<G, W, NBUF>(qp, kp, vp, block_table, ctx_lens, n_shards, out_o, out_lse, hq, hkv,
                          max_pages, num_pages, max_shards, chunks, n_units, units_per_xcd, batch,
-                         order, scale_log2, blockIdx.x, nullptr, nullptr, nullptr, pair_order);
+                         order, scale_log2, blockIdx.x, nullptr, nullptr, nullptr, unit_order);
 }
 
-// The dispatch order of a long-shard sweep over several requests: the (shard, request) pairs of
-// unit order (index r: request r % B, shard S_max - 1 - r / B) ranked by their page counts,
-// longest first, into order[0 .. B * S_max).  Workgroups are dispatched in index order and the
-// long shards' workgroups live long, so longest-first leaves the shortest shards, not whole
-// 256-page ones, for the end of the launch (longest-processing-time-first list scheduling); on a
-// ragged batch of 64 requests the sweep ends 4-5% sooner.  Counting sort in one workgroup over
-// kRankBuckets buckets of 2^shift pages: a histogram, its prefix sums (longest bucket first),
-// then every pair takes the next place of its bucket.  Pairs of one bucket keep no particular
-// order among themselves: the order decides only when a unit runs, never what it computes.
+// The XCD dealing cycle of rank_units_kernel: kXcdWeightEven : kXcdWeightOdd in lowest terms
+// (27 : 23), one cycle holding that many entries of every even and every odd XCD, spread by
+// smooth weighted round-robin so that every prefix of the cycle is near the weights.
+constexpr int kXcdCycleMax = 256;
+struct XcdCycle {
+  int len;
+  int count[8];                  // entries of XCD x in one cycle
+  uint8_t xcd[kXcdCycleMax];     // XCD of entry i
+  uint16_t before[kXcdCycleMax]; // entries of the same XCD before entry i
+};
+constexpr int gcd_of(int a, int b) { return b ? gcd_of(b, a % b) : a; }
+constexpr XcdCycle make_xcd_cycle() {
+  XcdCycle c{};
+  const int gd = gcd_of(kXcdWeightEven, kXcdWeightOdd);
+  const int we = kXcdWeightEven / gd, wo = kXcdWeightOdd / gd;
+  c.len = 4 * (we + wo);
+  int cur[8] = {};
+  for (int i = 0; i < c.len; ++i) {
+    int best = 0;
+    for (int x = 0; x < 8; ++x) cur[x] += (x & 1) ? wo : we;
+    for (int x = 1; x < 8; ++x)
+      if (cur[x] > cur[best]) best = x;
+    cur[best] -= c.len;
+    c.xcd[i] = (uint8_t)best;
+    c.before[i] = (uint16_t)c.count[best]++;
+  }
+  return c;
+}
+static_assert(kXcdWeightEven >= kXcdWeightOdd, "even XCDs take the larger share");
+constexpr int kXcdCycleLen = make_xcd_cycle().len;
+static_assert(kXcdCycleLen <= kXcdCycleMax, "XCD weights too fine for the cycle table");
+static_assert(kXcdCycleMax <= kRankBuckets && kRankBuckets % 8 == 0,
+              "the ordering kernel loads the cycle one entry per thread, fills queue t % 8");
+__constant__ XcdCycle kXcdCycle = make_xcd_cycle();
+
+// The dispatch order of an unchunked long-shard sweep, [8 * units_per_xcd] (workgroup index ->
+// unit, -1 for none).  Workgroups are dispatched in index order, index i on XCD i % 8, and the
+// long shards' workgroups live long, so
+//  * the (request, shard) pairs are ranked by page count, longest first: a request's shards are
+//    of one length, but across a ragged batch they differ 2x, and in shard-index order the last
+//    units to start were full-length shards that streamed alone at the end of the launch
+//    (longest-processing-time-first list scheduling);
+//  * the ranked units (all KV heads of a pair in turn) are dealt to the 8 XCDs' queues in the
+//    kXcdWeightEven : kXcdWeightOdd cycle, since the odd-numbered XCDs stream slower, when the
+//    even XCDs' queues hold that many (else round-robin); the empty units and the padding fill
+//    the rest of every queue.
+// Measured on a ragged batch of 64 requests: ranking -4% step time, the weighted dealing -2.4%
+// more.  Counting sort in one workgroup over kRankBuckets length buckets of 2^shift pages (the
+// last bucket holds the empty shards only); pairs of one bucket keep no particular order among
+// themselves.  The order decides only when and where a unit runs, never what it computes.
 __global__ void __launch_bounds__(kRankBuckets)
-rank_shards_kernel(const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ n_shards,
-                   int32_t batch, int32_t max_pages, int32_t max_shards, int32_t shift,
-                   int32_t* __restrict__ order) {
+rank_units_kernel(const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ n_shards,
+                  int32_t batch, int32_t max_pages, int32_t max_shards, int32_t hkv,
+                  int32_t units_per_xcd, int32_t shift, int32_t* __restrict__ unit_order) {
   __shared__ int32_t count[kRankBuckets];
   __shared__ int32_t scan[2][kRankBuckets];
-  const int t = threadIdx.x;
+  __shared__ int32_t ranked[kRankMaxPairs];  // pair index of rank r (unit order: r % B, S-1-r/B)
+  __shared__ uint16_t key[kRankMaxPairs];    // bucket of pair r
+  __shared__ uint8_t cyc_xcd[kXcdCycleMax];
+  __shared__ uint16_t cyc_before[kXcdCycleMax];
+  __shared__ int32_t cyc_count[8];
+  __shared__ int32_t s_live;
+  __shared__ int32_t used[8], first_free[8];
+  const int t = threadIdx.x, lane = t & 63;
   const int n_pairs = batch * max_shards;
-  // Bucket of pair r: longer shards get lower buckets.
-  auto bucket = [&](int r) {
-    const ShardRange range =
-        shard_range(ctx_lens, n_shards, r % batch, max_shards - 1 - r / batch, max_pages,
-                    max_shards);
-    return kRankBuckets - 1 - min((range.p1 - range.p0) >> shift, kRankBuckets - 1);
+  constexpr int cycle = kXcdCycleLen;
+  // x / hkv and x % hkv: a shift and a mask for the usual power-of-two head counts.
+  const int hkv_log2 = (hkv & (hkv - 1)) == 0 ? __builtin_ctz(hkv) : -1;
+  auto unit_of = [&](int rank, int j) {  // KV head j % hkv of the pair of rank rank + j / hkv
+    return hkv_log2 >= 0 ? ranked[rank + (j >> hkv_log2)] * hkv + (j & (hkv - 1))
+                         : ranked[rank + j / hkv] * hkv + j % hkv;
   };
+  if (t < cycle) {
+    cyc_xcd[t] = kXcdCycle.xcd[t];
+    cyc_before[t] = kXcdCycle.before[t];
+  }
+  if (t < 8) {
+    cyc_count[t] = kXcdCycle.count[t];
+    used[t] = 0;
+  }
   count[t] = 0;
   __syncthreads();
-  for (int r = t; r < n_pairs; r += kRankBuckets) atomicAdd(&count[bucket(r)], 1);
+  // Every pair's bucket, kept and counted.  Most pairs of a ragged batch are empty (slots past a
+  // request's shards): the empty bucket takes one atomic per wavefront.  (The loops run
+  // uniformly over the workgroup, so every ballot sees whole wavefronts.)
+  for (int r0 = 0; r0 < n_pairs; r0 += kRankBuckets) {
+    const int r = r0 + t;
+    int k = 0;
+    if (r < n_pairs) {
+      const ShardRange range = shard_range(ctx_lens, n_shards, r % batch,
+                                           max_shards - 1 - r / batch, max_pages, max_shards);
+      const int len = range.p1 - range.p0;
+      k = len == 0 ? kRankBuckets - 1 : kRankBuckets - 2 - min(len >> shift, kRankBuckets - 2);
+      key[r] = (uint16_t)k;
+    }
+    const bool empty = r < n_pairs && k == kRankBuckets - 1;
+    const uint64_t m = __ballot(empty);
+    if (r < n_pairs && !empty) atomicAdd(&count[k], 1);
+    if (lane == 0 && m != 0) atomicAdd(&count[kRankBuckets - 1], (int)__popcll(m));
+  }
   __syncthreads();
+  if (t == 0) s_live = n_pairs - count[kRankBuckets - 1];
   // Exclusive prefix sums of the counts (Hillis-Steele over the shifted counts).
   int cur = 0;
   scan[0][t] = t > 0 ? count[t - 1] : 0;
@@ -652,16 +725,72 @@ rank_shards_kernel(const int32_t* __restrict__ ctx_lens, const int32_t* __restri
     cur ^= 1;
     __syncthreads();
   }
-  count[t] = scan[cur][t];  // first place of bucket t
+  count[t] = scan[cur][t];  // first rank of bucket t
   __syncthreads();
-  for (int r = t; r < n_pairs; r += kRankBuckets) order[atomicAdd(&count[bucket(r)], 1)] = r;
+  for (int r0 = 0; r0 < n_pairs; r0 += kRankBuckets) {
+    const int r = r0 + t;
+    const int k = r < n_pairs ? key[r] : 0;
+    const bool empty = r < n_pairs && k == kRankBuckets - 1;
+    const uint64_t m = __ballot(empty);
+    int base = 0;
+    if (lane == 0 && m != 0) base = atomicAdd(&count[kRankBuckets - 1], (int)__popcll(m));
+    base = __shfl(base, 0);
+    if (r < n_pairs) {
+      const int at = empty ? base + (int)__popcll(m & ((1ull << lane) - 1))
+                           : atomicAdd(&count[k], 1);
+      ranked[at] = r;
+    }
+  }
+  __syncthreads();
+
+  // Live unit k (k < R) is KV head k % hkv of the pair of rank k / hkv.  Its XCD and place in that
+  // XCD's queue: entry k % cycle of the weighted cycle, or round-robin.
+  const int R = s_live * hkv;
+  const int full = R / cycle;
+  const bool weighted = (int64_t)(full + 1) * cyc_count[0] <= units_per_xcd;
+  if (weighted && t < R % cycle) atomicAdd(&used[cyc_xcd[t]], 1);
+  __syncthreads();
+  if (t < 8) used[t] += weighted ? full * cyc_count[t] : (R + 7 - t) / 8;
+  __syncthreads();
+  if (t == 0) {
+    int acc = 0;
+    for (int x = 0; x < 8; ++x) {
+      first_free[x] = acc;
+      acc += units_per_xcd - used[x];
+    }
+  }
+  __syncthreads();
+  for (int k = t; k < R; k += kRankBuckets) {
+    int x, pos;
+    if (weighted) {
+      const int i = k % cycle;
+      x = cyc_xcd[i];
+      pos = (k / cycle) * cyc_count[x] + cyc_before[i];
+    } else {
+      x = k & 7;
+      pos = k >> 3;
+    }
+    unit_order[8 * pos + x] = unit_of(0, k);
+  }
+  // The rest of every queue: empty unit e is KV head e % hkv of the pair of rank s_live + e / hkv
+  // (then -1).  Thread t fills queue t % 8 (kRankBuckets is a multiple of 8), places
+  // t / 8, t / 8 + 128, ... from the queue's first free one on.
+  const int n_empty = n_pairs * hkv - R;
+  const int x = t & 7;
+  constexpr int kStride = kRankBuckets / 8;
+  const int lo = used[x];
+  int pos = t >> 3;
+  if (pos < lo) pos += (lo - pos + kStride - 1) / kStride * kStride;
+  for (int e = first_free[x] + pos - lo; pos < units_per_xcd; pos += kStride, e += kStride)
+    unit_order[8 * pos + x] = e < n_empty ? unit_of(s_live, e) : -1;
 }
 
-// Fill p.pair_order (when the sweep has one) on `stream`, ahead of the sweep.
+// Fill p.unit_order (when the sweep has one) on `stream`, ahead of the sweep.
 hipError_t launch_rank(const SplitParams& p, hipStream_t stream) {
-  if (p.pair_order == nullptr) return hipSuccess;
-  hipLaunchKernelGGL(rank_shards_kernel, dim3(1), dim3(kRankBuckets), 0, stream, p.ctx_lens,
-                     p.n_shards, p.batch, p.max_pages, p.max_shards, p.rank_shift, p.pair_order);
+  if (p.unit_order == nullptr) return hipSuccess;
+  hipLaunchKernelGGL(rank_units_kernel, dim3(1), dim3(kRankBuckets), 0, stream, p.ctx_lens,
+                     p.n_shards, p.batch, p.max_pages, p.max_shards, p.hkv, p.units_per_xcd,
+                     p.rank_shift, p.unit_order);
   return hipGetLastError();
 }
 
@@ -702,7 +831,7 @@ hipError_t launch_gn(const SplitParams& p, hipStream_t stream) {
   hipLaunchKernelGGL((decode_split_kernel<G, kSplitWaves, NBUF>), dim3(grid), dim3(64 * kSplitWaves),
                      0, stream, p.q, p.k, p.v, p.block_table, p.ctx_lens, p.n_shards, p.out_o,
                      p.out_lse, p.hq, p.hkv, p.max_pages, p.num_pages, p.max_shards, p.chunks,
-                     p.n_units, p.units_per_xcd, p.batch, p.order, p.scale_log2, p.pair_order);
+                     p.n_units, p.units_per_xcd, p.batch, p.order, p.scale_log2, p.unit_order);
   return hipGetLastError();
 }
 
@@ -731,7 +860,7 @@ sweep_beside_linear_kernel(
     float* __restrict__ out_o, float* __restrict__ out_lse, int32_t hq, int32_t hkv,
     int32_t max_pages, int32_t num_pages, int32_t max_shards, int32_t chunks, int32_t n_units,
     int32_t units_per_xcd, int32_t batch, int32_t order, float scale_log2,
-    const int32_t* __restrict__ pair_order, const uint16_t* __restrict__ x,
+    const int32_t* __restrict__ unit_order, const uint16_t* __restrict__ x,
     const uint16_t* __restrict__ w,
     const uint16_t* __restrict__ gain, const uint16_t* __restrict__ residual,
     uint16_t* __restrict__ out_a, uint16_t* __restrict__ out_b, int32_t M, int32_t N, int32_t K,
@@ -745,7 +874,7 @@ sweep_beside_linear_kernel(
                                               out_lse, hq, hkv, max_pages, num_pages, max_shards,
                                               chunks, n_units, units_per_xcd, batch, order,
                                               scale_log2, 8u * before + lane8, nullptr, nullptr,
-                                              nullptr, pair_order);
+                                              nullptr, unit_order);
     return;
   }
   constexpr int U = 2, R = lin::beside_rows(MB), RG = lin::beside_rows_glu(MB);
@@ -780,7 +909,7 @@ hipError_t launch_beside(const SplitParams& p, const LinearParams& l, hipStream_
   hipLaunchKernelGGL((sweep_beside_linear_kernel<G, MB>), dim3(grid), dim3(64 * kSplitWaves), 0,
                      stream, p.q, p.k, p.v, p.block_table, p.ctx_lens, p.n_shards, p.out_o,
                      p.out_lse, p.hq, p.hkv, p.max_pages, p.num_pages, p.max_shards, p.chunks,
-                     p.n_units, p.units_per_xcd, p.batch, p.order, p.scale_log2, p.pair_order,
+                     p.n_units, p.units_per_xcd, p.batch, p.order, p.scale_log2, p.unit_order,
                      l.x, l.w, l.gain,
                      l.residual, l.out_a, l.out_b, l.M, l.N, l.K, l.n_split, l.eps, l.prologue,
                      l.glu ? 1 : 0, linear_groups);

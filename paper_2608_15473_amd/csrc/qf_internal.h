@@ -29,9 +29,11 @@ constexpr int kLongShardPages = 128;
 // XCDs (decode_split.hip): the odd XCDs stream slower.
 constexpr int kXcdWeightEven = 1080;
 constexpr int kXcdWeightOdd = 920;
-// Length buckets (and threads) of the one-workgroup kernel that ranks the shards of a long-shard
-// sweep over several requests by length (decode_split.hip).
+// The one-workgroup kernel that orders the units of an unchunked long-shard sweep
+// (decode_split.hip): length buckets (= its threads), and the most (request, shard) pairs it
+// ranks (held in LDS).
 constexpr int kRankBuckets = 1024;
+constexpr int kRankMaxPairs = 8192;
 
 // One launch of the sweep kernel.  A workgroup handles one unit (request b, shard s, chunk c,
 // KV head g); its output slot is [((b * max_shards + s) * chunks + c) * hq + g * G + h].
@@ -48,10 +50,11 @@ struct SplitParams {
   int32_t n_units;              // B * max_shards * chunks * Hkv
   int32_t units_per_xcd;        // ceil(n_units / 8)
   int32_t order;                // kOrderByRequest or kOrderByShardDesc (dispatch order of units)
-  // kOrderByShardDesc only, or null: [B * max_shards] int32 that a ranking kernel, launched just
-  // before the sweep, fills with the (shard, request) pairs in dispatch order, longest shard first
+  // kOrderByShardDesc with chunks == 1 only, or null: [8 * units_per_xcd] int32 that an ordering
+  // kernel, launched just before the sweep, fills with the unit each workgroup index sweeps (-1:
+  // none): longest shard first, dealt to the XCDs by kXcdWeightEven / kXcdWeightOdd
   // (rank_shift: log2 of the length buckets' width in pages).
-  int32_t* pair_order;
+  int32_t* unit_order;
   int32_t rank_shift;
   bool deep;                    // short shards of >= kDeepMinPages pages: split_buffers_deep(G)
   float scale_log2;             // softmax scale * log2(e)

@@ -81,10 +81,16 @@ int sweep_order(const qf_decode_desc* d, int64_t chunks) {
   return shard_pages >= qf::kLongShardPages ? qf::kOrderByShardDesc : qf::kOrderByRequest;
 }
 
-// A long-shard sweep over several requests ranks its (shard, request) pairs by length before it
-// starts (one int32 per pair of workspace); one request's shards are all of one length already.
-bool ranks_shards(const qf_decode_desc* d, int64_t chunks) {
-  return d->batch > 1 && sweep_order(d, chunks) == qf::kOrderByShardDesc;
+// An unchunked long-shard sweep (of up to kRankMaxPairs (request, shard) pairs) takes its units in
+// the order of rank_units_kernel, which it keeps in the workspace: one int32 per workgroup index.
+bool ranks_units(const qf_decode_desc* d, int64_t chunks) {
+  return chunks == 1 && sweep_order(d, chunks) == qf::kOrderByShardDesc &&
+         (int64_t)d->batch * d->max_shards <= qf::kRankMaxPairs;
+}
+size_t unit_order_bytes(const qf_decode_desc* d, int64_t chunks) {
+  if (!ranks_units(d, chunks)) return 0;
+  const int64_t units = (int64_t)d->batch * d->max_shards * d->n_kv_heads;
+  return (size_t)((units + 7) / 8 * 8) * sizeof(int32_t);
 }
 
 size_t chunk_state_bytes(const qf_decode_desc* d, int64_t chunks) {
@@ -93,10 +99,9 @@ size_t chunk_state_bytes(const qf_decode_desc* d, int64_t chunks) {
   return states * qf::kHeadDim * sizeof(float) + states * sizeof(float);
 }
 
-// qf_attn_decode_split's workspace: the chunk states, then the pair order.
+// qf_attn_decode_split's workspace: the chunk states or the unit order (never both).
 size_t workspace_bytes(const qf_decode_desc* d, int64_t chunks) {
-  const size_t order = ranks_shards(d, chunks) ? (size_t)d->batch * d->max_shards * sizeof(int32_t) : 0;
-  return chunk_state_bytes(d, chunks) + order;
+  return chunk_state_bytes(d, chunks) + unit_order_bytes(d, chunks);
 }
 
 // Everything qf_attn_decode_split checks and derives before launching.
@@ -110,8 +115,8 @@ struct Split {
 };
 
 // fold: the chunks are folded into part_out / part_lse (chunk states in the workspace) or left
-// as slots there; rank: the workspace also holds the pair order of a ranked sweep.  The workspace
-// is needed for whichever of the two applies.
+// as slots there; rank: the workspace holds the unit order of a ranked sweep.  The workspace is
+// needed for whichever of the two applies.
 int prepare_split(const qf_decode_desc* desc, const void* q, const void* k_cache,
                   const void* v_cache, const int32_t* block_table, const int32_t* ctx_lens,
                   const int32_t* n_shards, float* part_out, float* part_lse, void* workspace,
@@ -136,8 +141,8 @@ int prepare_split(const qf_decode_desc* desc, const void* q, const void* k_cache
 
   const int64_t chunks = choose_chunks(&d);
   const size_t state_bytes = fold ? chunk_state_bytes(&d, chunks) : 0;
-  rank = rank && ranks_shards(&d, chunks);
-  const size_t need = state_bytes + (rank ? (size_t)d.batch * d.max_shards * sizeof(int32_t) : 0);
+  const size_t need = state_bytes + (rank ? unit_order_bytes(&d, chunks) : 0);
+  rank = need > state_bytes;
   if (need) {
     if (!workspace) return fail(QF_EINVAL, "this shape needs %zu bytes of workspace", need);
     if (workspace_size < need)
@@ -173,7 +178,7 @@ int prepare_split(const qf_decode_desc* desc, const void* q, const void* k_cache
   p.units_per_xcd = (int32_t)((units + 7) / 8);
   const int64_t shard_pages = (d.max_pages_per_seq + d.max_shards - 1) / d.max_shards / chunks;
   p.order = sweep_order(&d, chunks);
-  p.pair_order = rank ? reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + state_bytes)
+  p.unit_order = rank ? reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + state_bytes)
                       : nullptr;
   p.rank_shift = 0;
   while ((d.max_pages_per_seq >> p.rank_shift) >= qf::kRankBuckets) ++p.rank_shift;

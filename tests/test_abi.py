@@ -82,10 +82,13 @@ def test_bad_descriptor_is_rejected(kw, code):
 
 
 def _order_bytes(d, chunks):
-    """The header's rule for the dispatch order in the workspace: a batch of several requests
-    whose shards (or chunks) are 128+ pages long at full capacity ranks its B * S_max pairs."""
-    long = -(-d.max_pages_per_seq // d.max_shards) // chunks >= 128
-    return 4 * d.batch * d.max_shards if d.batch > 1 and long else 0
+    """The header's rule for the dispatch order in the workspace: an unchunked shape whose shards
+    are 128+ pages long at full capacity, with at most 8,192 (request, shard) pairs, keeps one
+    int32 per workgroup index (the units rounded up to a multiple of 8)."""
+    long = -(-d.max_pages_per_seq // d.max_shards) >= 128
+    units = d.batch * d.max_shards * d.n_kv_heads
+    ranked = chunks == 1 and long and d.batch * d.max_shards <= 8192
+    return 4 * (-(-units // 8) * 8) if ranked else 0
 
 
 def test_workspace_only_when_units_are_few_or_shards_are_ranked():
@@ -95,10 +98,15 @@ def test_workspace_only_when_units_are_few_or_shards_are_ranked():
     assert rc == 0 and n > 0                               # chunk states
     assert n % 16 == 0
     rc, n = _ws(_desc(batch=48, max_shards=16, max_pages_per_seq=2560, num_pages=65536))
-    assert rc == 0 and n == 48 * 16 * 4                    # 160-page shards: the order only
+    assert rc == 0 and n == 48 * 16 * 8 * 4                # 160-page shards: the order only
     rc, n = _ws(_desc(batch=64, n_q_heads=32, max_shards=32, max_pages_per_seq=8192,
                       num_pages=140000))
-    assert rc == 0 and n == 64 * 32 * 4                    # the ragged 64-request batch
+    assert rc == 0 and n == 64 * 32 * 8 * 4                # the ragged 64-request batch
+    rc, n = _ws(_desc(batch=3, n_q_heads=3, n_kv_heads=3, max_shards=87, max_pages_per_seq=20000,
+                      num_pages=65536))
+    assert rc == 0 and n == 784 * 4                        # 783 units, rounded up to 8
+    rc, n = _ws(_desc(batch=8193, max_shards=1, max_pages_per_seq=128, num_pages=1 << 21))
+    assert rc == 0 and n == 0                              # too many pairs to rank
 
 
 def _chunks(**kw):

@@ -2,8 +2,8 @@
 
 Shapes with many (request, shard, KV head) units whose shards are long (128+ pages per shard at full
 capacity) are swept longest shard first, one workgroup per unit: the split sweep ranks the
-(request, shard) pairs by length in its workspace before it starts, the unfolded sweep (no
-workspace) takes them by shard index, descending.  Every output of every case is checked:
+(request, shard) pairs by length and deals their units to the XCDs in its workspace before it
+starts, the unfolded sweep (no workspace) takes them by shard index, descending.  Every output of every case is checked:
 per-shard partials and the combined result, at every group size, including requests with no
 positions, partial last pages, more shards than pages, very little work in all, one long request
 next to many short ones, out-of-range device values, the unfolded sweep followed by the combine
@@ -26,12 +26,12 @@ def _desc(case):
 
 def _is_long_shard_shape(case):
     """128+ pages per shard at full capacity and at least one full set of resident workgroups'
-    worth of units (no sub-shard chunks); the split sweep then ranks the B * S_max (request,
-    shard) pairs, and its workspace is that order."""
+    worth of units (no sub-shard chunks); the split sweep then takes its units in a ranked
+    order, one int32 per workgroup index in its workspace."""
     B, S = case.q.shape[0], case.max_shards
     long = -(-case.block_table.shape[1] // S) >= 128
     desc = _desc(case)
-    ranked = qf.workspace_size(desc) == 4 * B * S
+    ranked = qf.workspace_size(desc) == 4 * (-(-B * S * case.k_cache.shape[1] // 8) * 8)
     return long and qf.split_chunks(desc) == 1 and ranked
 
 
