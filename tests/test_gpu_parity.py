@@ -396,8 +396,8 @@ def _one_launch_vs_two(case, workspace=None, counters=None):
     out1, lse1 = qf.attn_decode(*args, max_shards=case.max_shards, scale=case.scale,
                                 workspace=workspace, counters=counters)
     torch.cuda.synchronize()
-    chunked = qf.workspace_size(qf.make_desc(case.q, case.k_cache, case.block_table,
-                                             case.max_shards, case.scale)) > 0
+    chunked = qf.split_chunks(qf.make_desc(case.q, case.k_cache, case.block_table,
+                                           case.max_shards, case.scale)) > 1
     if not chunked and case.max_shards <= 64:
         assert torch.equal(_bits(out1), _bits(out2))
         assert torch.equal(_bits(lse1), _bits(lse2))
