@@ -56,10 +56,12 @@ __device__ __forceinline__ void merge_row(
   const float2* o = reinterpret_cast<const float2*>(in_o + ((size_t)r * entries * hq + h) * D) + lane;
   const size_t o_step = (size_t)hq * D / 2;  // float2 between entries
 
-  // Wavefront w takes entries [K w, K w + K) of every K W.  Its K log-partitions and O rows are
-  // all loaded before any is used, so a row costs one memory round trip; each wavefront keeps its
-  // own running maximum m_w (rescaling its sums when a later group raises it), and the wavefronts
+  // Wavefront w takes entries [K w, K w + K) of every K W: its K log-partitions, then the O rows
+  // of the live ones among them, all loaded before any is used.  Each wavefront keeps its own
+  // running maximum m_w (rescaling its sums when a later group raises it), and the wavefronts
   // meet in LDS, where every sum is rescaled by exp(m_w - m).  Empty entries are selected out.
+  // (Loading every O row together with the log-partitions, one round trip instead of two, was
+  // measured slower on MI355X, also where every entry is live.)
   constexpr int K = 16;
   float m_w = -INFINITY;
   float L = 0.0f;
