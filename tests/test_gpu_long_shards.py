@@ -62,6 +62,17 @@ def test_long_shards_every_group_size(gpu, G):
         assert np.all(got["part_lse"][b, S[b]:] == -np.inf)
 
 
+def test_long_shards_three_kv_heads(gpu):
+    """A KV head count that is not a power of two (the dispatch order's unit arithmetic then
+    divides instead of shifting), every output checked."""
+    n, S = _ragged(48, 470)
+    case = make_case(48, 6, 3, n, S, seed=470, max_shards=16, max_pages=2560, device=gpu)
+    assert _is_long_shard_shape(case)
+    say("[long shards] three KV heads")
+    got = run_gpu(case)
+    check(case, got, oracle_ref(case), label="long shards, 3 KV heads")
+
+
 def test_long_shards_with_little_work(gpu):
     """Few pages in all (most units empty or of a few pages), and one request whose single shard
     is 100 times longer than the others."""
