@@ -35,6 +35,14 @@ WORKLOAD_LABELS = {
 }
 
 
+# The decode-stage workloads (bench.py --stage), their names in the tables.
+STAGE_LABELS = {
+    "qwen3-0.6b_stage_b1_n4608": "Qwen3-0.6B, 1 request, 4,608 tokens, 24 shards, 28 blocks",
+    "qwen3-4b_stage_b1_n36480": "Qwen3-4B, 1 request, 36,480 tokens, 128 shards, 36 blocks",
+    "qwen3-0.6b_stage_b8_n4608": "Qwen3-0.6B, 8 requests, 4,608 tokens, 16 shards, 28 blocks",
+}
+
+
 def source_digest() -> str:
     """sha256 over every source a measurement depends on: the library's sources, its header, the
     bench and the input generator (the same digest bench.py stamps on each result)."""
@@ -48,12 +56,14 @@ def source_digest() -> str:
     return h.hexdigest()
 
 
-def load_records() -> dict:
+def load_records(stage: bool = False) -> dict:
+    """{workload: runs} of the decode-attention records, or (stage) of the decode-stage ones
+    (whose lines carry per-kernel times)."""
     recs = {}
     for path in sorted(glob.glob(os.path.join(RECORDS, "bench_*.json"))):
         with open(path) as f:
             rec = json.load(f)
-        runs = [r for r in rec["runs"] if "kernels" not in r]   # decode-attention runs only
+        runs = [r for r in rec["runs"] if ("kernels" in r) == stage]
         if runs:
             recs[rec["workload"]] = runs
     return recs
@@ -122,7 +132,61 @@ def design_table(recs, digest) -> str:
     return "\n".join(rows)
 
 
-TABLES = {("README.md", "readme"): readme_table, ("DESIGN.md", "design"): design_table}
+def stage_table(recs, digest) -> str:
+    rows = ["| workload | serial ms/step | two HIP streams | shared launch (tokens/s) | sweep alone | "
+            "shared vs serial (sweep hidden) | shared launch kernel: µs, GB/s (% of 8 TB/s) | "
+            "fp64 oracle on the host | runs (sources) |",
+            "|---|---|---|---|---|---|---|---|---|"]
+    for name, label in STAGE_LABELS.items():
+        if name not in recs:
+            continue
+        runs, cur = _current(recs[name], digest)
+        f3 = lambda v: f"{v:.3f}"
+        serial = _span([r["serial_ms_per_step"] for r in runs], f3)
+        streams = _span([r["streams_ms_per_step"] for r in runs], f3)
+        fused = _span([r["fused_ms_per_step"] for r in runs], f3)
+        tps = _span([r["value"] for r in runs], lambda v: f"{v:,.0f}")
+        alone = _span([r["sweep_only_ms_per_step"] for r in runs], f3)
+        speed = _span([r["speedup_vs_serial"] for r in runs], lambda v: f"{v:.2f}×")
+        hidden = _span([100 * r["sweep_hidden_frac"] for r in runs], lambda v: f"{v:.0f}%")
+        us = _span([r["roofline"]["launch_avg_us"] for r in runs], lambda v: f"{v:.1f}")
+        gbs = _span([r["roofline"]["achieved"] for r in runs], lambda v: f"{v:,.0f}")
+        pct = _span([100 * r["roofline"]["frac"] for r in runs], lambda v: f"{v:.0f}")
+        cpus = [r["cpu_baseline"] for r in runs if "cpu_baseline" in r]
+        cpu = (f"{_span([c['value'] for c in cpus], lambda v: f'{v:.3g}')} tokens/s"
+               if cpus else "—")
+        srcs = sorted({r.get("env", {}).get("source_sha256", "")[:8] for r in runs})
+        rows.append(f"| {label} | {serial} | {streams} | **{fused}** ({tps}) | {alone} | "
+                    f"{speed} ({hidden}) | {us}, {gbs} ({pct}%) | {cpu} | "
+                    f"{len(runs)} ({', '.join(srcs)}{'' if cur else ', earlier'}) |")
+    return "\n".join(rows)
+
+
+def readme_stage(recs, digest) -> str:
+    """One sentence on the decode stage, its numbers from the stage records."""
+    def step(name):
+        runs, _ = _current(recs[name], digest)
+        ms = _span([r["fused_ms_per_step"] for r in runs], lambda v: f"{v:.2f}")
+        tps = _span([r["value"] for r in runs], lambda v: f"{v:,.0f}")
+        return ms, tps
+    parts = []
+    if "qwen3-0.6b_stage_b1_n4608" in recs:
+        ms, tps = step("qwen3-0.6b_stage_b1_n4608")
+        parts.append(f"a batch-1 Qwen3-0.6B step at 4,608 tokens in {ms} ms ({tps} tokens/s")
+        if "qwen3-0.6b_stage_b8_n4608" in recs:
+            parts[-1] += f"; eight requests: {step('qwen3-0.6b_stage_b8_n4608')[1]} tokens/s"
+        parts[-1] += ")"
+    if "qwen3-4b_stage_b1_n36480" in recs:
+        ms, tps = step("qwen3-4b_stage_b1_n36480")
+        parts.append(f"a batch-1 Qwen3-4B step at 36,480 tokens in {ms} ms ({tps} tokens/s)")
+    if not parts:
+        return ""
+    return ("The decode stage (`bench.py --stage`, every block of the model with the sweep beside "
+            "the feed-forward) runs " + " and ".join(parts) + ".")
+
+
+TABLES = {("README.md", "readme"): readme_table, ("DESIGN.md", "design"): design_table,
+          ("DESIGN.md", "stage"): stage_table, ("README.md", "readme-stage"): readme_stage}
 
 
 def _replace(text, tag, body):
@@ -133,14 +197,17 @@ def _replace(text, tag, body):
     return text[:i + len(begin)] + "\n" + body + "\n" + text[j:]
 
 
+STAGE_TAGS = ("stage", "readme-stage")
+
+
 def render() -> dict:
     """{file: new text} with every table regenerated from the records."""
-    recs, digest = load_records(), source_digest()
+    recs, stage_recs, digest = load_records(), load_records(stage=True), source_digest()
     out = {}
     for (fname, tag), fn in TABLES.items():
         path = os.path.join(ROOT, fname)
         text = out.get(fname) or open(path).read()
-        out[fname] = _replace(text, tag, fn(recs, digest))
+        out[fname] = _replace(text, tag, fn(stage_recs if tag in STAGE_TAGS else recs, digest))
     return out
 
 

@@ -32,7 +32,16 @@ def test_records_are_complete_and_consistent(fname, workload, run):
     env = run["env"]
     for key in ("source_sha256", "rocm", "hip", "torch", "gpu", "cpu_model", "host_cores"):
         assert env.get(key), key
-    if "kernels" in run:        # a decode-stage record
+    if "kernels" in run:        # a decode-stage record: tokens/s, speedup and hidden share
+        fused, serial = run["fused_ms_per_step"], run["serial_ms_per_step"]
+        tps = run["config"]["batch"] / (fused / 1e3)
+        assert abs(tps - run["value"]) <= tps * (1e-3 + 0.5e-4 / fused)
+        assert abs(serial / fused - run["speedup_vs_serial"]) <= 2e-3 * serial / fused
+        hidden = (serial - fused) / run["sweep_only_ms_per_step"]
+        assert abs(hidden - run["sweep_hidden_frac"]) <= 2e-3
+        roof = run["roofline"]
+        assert roof["kernel"] in run["kernels"]
+        assert abs(roof["achieved"] / roof["peak"] - roof["frac"]) <= 1e-3
         return
     # value = KV bytes per step / step time; the roofline fraction = achieved / peak
     ms = run["ms_per_step"]
