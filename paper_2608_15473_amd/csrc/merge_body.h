@@ -61,7 +61,7 @@ __device__ __forceinline__ void merge_row(
   // running maximum m_w (rescaling its sums when a later group raises it), and the wavefronts
   // meet in LDS, where every sum is rescaled by exp(m_w - m).  Empty entries are selected out.
   // (Loading every O row together with the log-partitions, one round trip instead of two, was
-  // measured slower on MI355X, also where every entry is live.)
+  // measured no faster on MI355X, also where every entry is live.)
   constexpr int K = 16;
   float m_w = -INFINITY;
   float L = 0.0f;
