@@ -127,7 +127,7 @@ RESIDENT = {1: 1024, 2: 768, 4: 768, 8: 512}
 
 def _one_unit_chunks(G):
     """Chunks of one (request, shard, KV head) unit of 2^20 positions: one per resident
-    workgroup (the page cap, 8,192 at two pages per wavefront, and the 1,024 cap do not bind)."""
+    workgroup (the page cap, 5,461 at three pages per wavefront, and the 1,024 cap do not bind)."""
     return _chunks(batch=1, n_q_heads=G, n_kv_heads=1, max_shards=1, max_pages_per_seq=65536,
                    num_pages=65536)
 
@@ -135,13 +135,13 @@ def _one_unit_chunks(G):
 def test_chunks_fill_one_set_of_resident_workgroups():
     """Without a GPU to ask, the library assumes the MI355X's resident sweep workgroups (768 at
     G = 2): the 1M-token shape's 128 units take 6 chunks (768 workgroups), whose states are
-    B * S * C * Hq * (128 + 1) fp32; a wavefront keeps at least 2 pages (C <= pages / 8), and
+    B * S * C * Hq * (128 + 1) fp32; a wavefront keeps at least 3 pages (C <= pages / 12), and
     shapes with at least 768 units take none.  (On a GPU the count comes from its occupancy.)"""
     import torch
     if torch.cuda.is_available():
         pytest.skip("the resident-workgroup count is the device's own here")
     assert _chunks(batch=1, max_shards=16, max_pages_per_seq=65536, num_pages=65536) == 6
-    assert _chunks(batch=1, max_shards=8, max_pages_per_seq=288, num_pages=288) == 4    # 36 pages
+    assert _chunks(batch=1, max_shards=8, max_pages_per_seq=288, num_pages=288) == 3    # 36 pages
     assert _chunks(batch=3, max_shards=32, max_pages_per_seq=65536, num_pages=65536) == 0  # 768
     for G, resident in RESIDENT.items():
         assert _one_unit_chunks(G) == resident, G
