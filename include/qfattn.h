@@ -160,7 +160,7 @@ int qf_attn_decode_split_unfolded(const qf_decode_desc* desc, const void* q, con
  * buffers.  Bitwise the same when the shape needs no sub-shard chunks
  * (qf_attn_decode_split_chunks() == 1) and max_shards <= 64; otherwise the slots are
  * grouped differently (the chunks of every shard merge in the same pass as the shards; more than
- * 64 slots are summed by 4 wavefronts instead of 16), which can move the last bits.  The last
+ * 64 slots are summed by 4 wavefronts instead of 8 or 16), which can move the last bits.  The last
  * workgroup to finish a (request, KV head) merges that group's slots (partial states stay in the
  * workspace), so the merge's launch and its wait for the sweep's tail disappear.  Being one
  * launch, it sweeps long shards in their plain order (no ranked dispatch order).

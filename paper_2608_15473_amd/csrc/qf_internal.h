@@ -18,7 +18,6 @@ constexpr int kSplitWaves = 4;    // waves per workgroup of the sweep kernel
 constexpr int kSplitBuffers = 2;
 constexpr int split_buffers_deep(int group) { return group <= 2 ? 5 : group == 4 ? 3 : 2; }
 constexpr int kDeepMinPages = 4 * kSplitWaves;   // shard pages (at full capacity) for deep buffers
-constexpr int kMergeWaves = 4;    // waves per workgroup of the merge kernel
 
 // Dispatch orders of the sweep's units (see decode_split.hip).
 constexpr int kOrderByRequest = 0;

@@ -217,7 +217,7 @@ def test_planted_secondary_reading(gpu):
 
 
 def test_many_shard_slots_and_many_chunks(gpu):
-    """Rows of more than 64 slots (the merge's 16-wavefront form): 256 shard slots merged by the
+    """Rows of more than 128 slots (the merge's 16-wavefront form): 256 shard slots merged by the
     combine, and one unit of a long cache cut into hundreds of chunks merged into its shard."""
     case = make_case(2, 16, 8, [3000, 70000], [150, 200], seed=175, max_shards=256, device=gpu)
     _run(case, "256 shard slots")
