@@ -171,3 +171,36 @@ def test_long_shards_beside_a_product_equal_the_two_calls_bitwise(gpu):
     for a, b in zip(*outs):
         assert torch.equal(a, b)
     assert not torch.isnan(outs[1][1].view(torch.float32)).any()
+
+
+def test_long_shards_plan_replayed_from_a_graph(gpu):
+    """The ordering kernel and the sweep and combine of a plan, captured in a HIP graph: every
+    replay (with eager work on other buffers between replays) equals the eager call bitwise."""
+    n, S = _ragged(48, 480)
+    case = make_case(48, 16, 8, n, S, seed=480, max_shards=16, max_pages=2560, device=gpu)
+    assert _is_long_shard_shape(case)
+    args = (case.q, case.k_cache, case.v_cache, case.block_table, case.ctx_lens, case.n_shards)
+    st = torch.cuda.Stream()                         # the plan's stream, captured below
+    plan = qf.DecodeStepPlan(*args, max_shards=16, scale=case.scale, fold_chunks=False,
+                             stream=st.cuda_stream)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(st):
+        out, lse = plan()
+    torch.cuda.synchronize()
+    eager = (out.view(torch.int16).clone(), lse.view(torch.int32).clone(),
+             plan.part_lse.view(torch.int32).clone())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=st):
+        plan.split()
+        plan.combine()
+    other = make_case(4, 16, 8, [3000, 17, 0, 900], [2, 1, 1, 3], seed=481, device=gpu)
+    for r in range(3):
+        plan.out.fill_(float("nan"))
+        plan.part_lse.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        say(f"[long shards] graph replay {r}")
+        assert torch.equal(plan.out.view(torch.int16), eager[0])
+        assert torch.equal(plan.lse.view(torch.int32), eager[1])
+        assert torch.equal(plan.part_lse.view(torch.int32), eager[2])
+        run_gpu(other)                                   # eager work between replays
