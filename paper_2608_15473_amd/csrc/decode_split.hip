@@ -197,8 +197,9 @@ __device__ __forceinline__ void sweep_unit(
   //    weighted by that parity (kXcdWeightEven / kXcdWeightOdd): measured on MI355X, odd-numbered
   //    XCDs stream 8-17% slower than even ones under the long-shard sweep, whatever KV head they
   //    read, so equal chunks leave the even XCDs idle while the odd ones finish.
-  //    Without chunks, a unit order (rank_units_kernel) replaces both: each workgroup index
-  //    names its unit, longest shard first, and the odd XCDs get fewer of the long units.
+  //    Without chunks (and with at most kRankMaxPairs (request, shard) pairs), a unit order
+  //    written by rank_units_kernel replaces both: each workgroup index names its unit, longest
+  //    shard first, and the odd XCDs get fewer of the long units.
   int g, c, s, b;
   int pair = 0;  // long shards with chunks: index of the (request, shard, KV head) in unit order
   if (order == kOrderByRequest) {
