@@ -118,22 +118,24 @@ int qf_attn_decode_split(const qf_decode_desc* desc, const void* q, const void* 
 
 /*
  * Sub-shard chunks per shard that the sweep uses for this shape (host call): C >= 1; C > 1 exactly
- * when qf_attn_decode_split_workspace_size() is nonzero (few (request, KV head, shard) units:
- * the pages of every shard are cut into C consecutive ranges, so that the sweep fills the GPU
- * once).  Shards shorter than 128 pages at full capacity get ranges of ceil(len / C) pages, len
- * the shard's page count, the last ranges shorter or empty; longer shards get ranges whose sizes
- * alternate between two weights (1080 : 920), because their chunks alternate between the
- * even- and odd-numbered XCDs of the device and the odd ones stream slower.  Any partition gives
- * the same merged attention (§5).  Like the workspace size, C depends on the device's resident
- * workgroups.  Returns QF_OK, QF_EINVAL or QF_EUNSUPPORTED.
+ * when the shape has fewer (request, KV head, shard) units than the sweep keeps resident on the
+ * GPU at once (the workspace then holds the chunks' partial states): the pages of every shard are
+ * cut into C consecutive ranges, so that the sweep fills the GPU once, each range keeping at
+ * least 3 pages per wavefront.  Where a chunk would hold fewer than 128 pages at full capacity
+ * (ceil(max_pages_per_seq / max_shards) / C < 128) the ranges are ceil(len / C) pages, len the
+ * shard's page count, the last ones shorter or empty; otherwise their sizes alternate between two
+ * weights (1080 : 920), because the chunks alternate between the even- and odd-numbered XCDs of
+ * the device and the odd ones stream slower.  Any partition gives the same merged attention
+ * (§5).  Like the workspace size, C depends on the device's resident workgroups.  Returns QF_OK,
+ * QF_EINVAL or QF_EUNSUPPORTED.
  */
 int qf_attn_decode_split_chunks(const qf_decode_desc* desc, int32_t* chunks);
 
 /*
  * The sweep of qf_attn_decode_split without folding the sub-shard chunks into their shards: slot
  * s * C + c of request b receives the pair (O, ln Z) of chunk c of shard s, C =
- * qf_attn_decode_split_chunks() (with C == 1 the slots are the shards and this call is
- * qf_attn_decode_split).  A chunk is itself a shard of a finer split of the same cache (§5: any
+ * qf_attn_decode_split_chunks() (with C == 1 the slots are the shards and the results are
+ * qf_attn_decode_split's, bit for bit).  A chunk is itself a shard of a finer split of the same cache (§5: any
  * partition), so qf_attn_combine over the max_shards * C slots gives the result of the folded
  * sweep followed by the combine, up to the order of the fp32 sums, with one launch fewer and no
  * workspace: for callers that need only the merged attention, not per-shard partials.  Having no

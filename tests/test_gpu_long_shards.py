@@ -204,3 +204,56 @@ def test_long_shards_plan_replayed_from_a_graph(gpu):
         assert torch.equal(plan.lse.view(torch.int32), eager[1])
         assert torch.equal(plan.part_lse.view(torch.int32), eager[2])
         run_gpu(other)                                   # eager work between replays
+
+
+def _shard_pages(n, S, s, max_pages, max_shards):
+    """Pages of shard s of a request with n positions cut into S shards (the header's split
+    rule; out-of-range values clamped as the kernels clamp them)."""
+    n = min(max(int(n), 0), max_pages * 16)
+    S = min(max(int(S), 1), max_shards)
+    pages = -(-n // 16)
+    per = -(-pages // S)
+    return min((s + 1) * per, pages) - min(s * per, pages) if s < S else 0
+
+
+def test_long_shards_dispatch_order(gpu):
+    """The dispatch order the ordering kernel leaves in the workspace (white box): workgroup
+    index i runs unit order[i] on XCD i % 8; every unit appears exactly once and the rest is -1;
+    along each XCD's queue the live units come first, longest shard first (to the kernel's
+    length buckets of 2^shift pages), then the empty ones; and the even XCDs get at least as many
+    live units as the odd ones."""
+    n, S = _ragged(48, 490)
+    B, Hkv, smax, maxp = 48, 8, 16, 2560
+    case = make_case(B, 16, Hkv, n, S, seed=490, max_shards=smax, max_pages=maxp, device=gpu)
+    assert _is_long_shard_shape(case)
+    desc = _desc(case)
+    units = B * smax * Hkv
+    ws = torch.empty(qf.workspace_size(desc), dtype=torch.uint8, device=gpu)
+    qf.attn_decode_split(case.q, case.k_cache, case.v_cache, case.block_table, case.ctx_lens,
+                         case.n_shards, max_shards=smax, scale=case.scale, workspace=ws)
+    torch.cuda.synchronize()
+    order = ws.view(torch.int32).cpu().numpy()
+    say("[long shards] dispatch order")
+    assert len(order) == -(-units // 8) * 8
+    live_vals = order[order >= 0]
+    assert np.all(order >= -1) and np.array_equal(np.sort(live_vals), np.arange(units))
+    shift = 0
+    while (maxp >> shift) >= 1024:
+        shift += 1
+    ctx = case.ctx_lens.cpu().numpy()
+    ns = case.n_shards.cpu().numpy()
+
+    def pages(u):                       # unit u = pair * Hkv + g, pair r: request r % B,
+        r = u // Hkv                    # shard smax - 1 - r // B
+        return _shard_pages(ctx[r % B], ns[r % B], smax - 1 - r // B, maxp, smax)
+
+    live_per_xcd = []
+    for x in range(8):
+        q = [int(u) for u in order[x::8] if u >= 0]
+        p = np.array([pages(u) for u in q])
+        live = int(np.sum(p > 0))
+        assert np.all(p[:live] > 0) and np.all(p[live:] == 0), x      # live units first
+        assert np.all(np.diff(p[:live] >> shift) <= 0), x              # longest first
+        live_per_xcd.append(live)
+    assert sum(live_per_xcd) == sum(1 for u in range(units) if pages(u) > 0)
+    assert min(live_per_xcd[0::2]) >= max(live_per_xcd[1::2]), live_per_xcd
