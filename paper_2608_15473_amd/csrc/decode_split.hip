@@ -116,6 +116,120 @@ __device__ __forceinline__ void unpack8(const uint4& w, float* f) {
 // until its own stores have completed before the workgroup barrier, and the count is a
 // device-scope atomic.  The last unit then sets the counter back to 0 for the next call.
 // Nothing ever waits for another workgroup.
+// The G query heads of one (request, KV head) merged over their `entries` slots by the last unit
+// of the group.  When one 16-slot group per wavefront covers the slots with W / G wavefronts per
+// head (or W / 2, ...), heads are merged side by side by teams of wavefronts, and every wavefront
+// loads its log-partitions and O rows at once (one memory round trip; the O rows of empty slots
+// are read and discarded); each team sums exactly what merge_row's wavefronts sum, in the same
+// order, so the bits are merge_row's.  Otherwise head by head with merge_row.  The partial states
+// were written by other workgroups of this launch: read with device-scope loads.
+template <int G, int W>
+__device__ __forceinline__ void merge_group(const float* __restrict__ part_o,
+                                            const float* __restrict__ part_lse,
+                                            uint16_t* __restrict__ merged_o,
+                                            float* __restrict__ merged_lse, int b, int g, int hq,
+                                            int entries) {
+  constexpr int K = 16;
+  const int groups = (entries + K - 1) / K;
+  const int hpw = min(G, W / max(groups, 1));   // heads merged side by side
+  if (hpw < 2) {
+#pragma unroll 1
+    for (int h = 0; h < G; ++h)
+      mrg::merge_row<true, false, W, true>(part_o, part_lse, merged_o, merged_lse, entries, hq, b,
+                                           g * G + h, nullptr, nullptr, nullptr, 1, 0.0f);
+    return;
+  }
+  const int wph = W / hpw;                       // wavefronts per head, >= groups
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int sub = wave / wph, wl = wave % wph;
+  __shared__ float2 s_acc[W][64];
+  __shared__ float s_L[W];
+  __shared__ float s_m[W];
+  __shared__ int s_nan[W];
+#pragma unroll 1
+  for (int h0 = 0; h0 < G; h0 += hpw) {
+    const int h = g * G + h0 + min(sub, hpw - 1);
+    const float* lse = part_lse + (size_t)b * entries * hq + h;
+    const float* o = part_o + ((size_t)b * entries * hq + h) * mrg::D + 2 * lane;
+    const size_t o_step = (size_t)hq * mrg::D;
+    float x[K];
+    uint64_t raw[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int i = K * wl + k;
+      const bool in = sub < hpw && i < entries;
+      x[k] = in ? __hip_atomic_load(&lse[(size_t)i * hq], __ATOMIC_RELAXED,
+                                    __HIP_MEMORY_SCOPE_AGENT)
+                : -INFINITY;
+      raw[k] = in ? __hip_atomic_load(reinterpret_cast<const uint64_t*>(o + i * o_step),
+                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                  : 0ull;
+    }
+    // This wavefront's group, as one round of merge_row's loop.
+    float m_w = -INFINITY, L = 0.0f;
+    float2 acc = make_float2(0.0f, 0.0f);
+    bool nan = false;
+    float mc = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      nan |= (x[k] != x[k]);
+      mc = fmaxf(mc, x[k]);
+    }
+    if (mc != -INFINITY) {
+      m_w = mc;
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const float w = (x[k] == -INFINITY) ? 0.0f : expf(x[k] - m_w);
+        const float2 v = __builtin_bit_cast(float2, raw[k]);
+        L += w;
+        acc.x = (w == 0.0f) ? acc.x : fmaf(w, v.x, acc.x);
+        acc.y = (w == 0.0f) ? acc.y : fmaf(w, v.y, acc.y);
+      }
+    }
+    s_acc[wave][lane] = acc;
+    if (lane == 0) {
+      s_L[wave] = L;
+      s_m[wave] = m_w;
+      s_nan[wave] = nan;
+    }
+    __syncthreads();
+    if (sub < hpw && wl == 0) {   // the team's first wavefront: merge_row's final merge
+      const int w0 = sub * wph;
+      float M = s_m[w0];
+      bool any_nan = s_nan[w0];
+      for (int w = 1; w < wph; ++w) {
+        M = fmaxf(M, s_m[w0 + w]);
+        any_nan |= s_nan[w0 + w];
+      }
+      float2 a = make_float2(0.0f, 0.0f);
+      float Lt = 0.0f;
+      for (int w = 0; w < wph; ++w) {
+        const float f = (s_m[w0 + w] == -INFINITY) ? 0.0f : expf(s_m[w0 + w] - M);
+        a.x = fmaf(f, s_acc[w0 + w][lane].x, a.x);
+        a.y = fmaf(f, s_acc[w0 + w][lane].y, a.y);
+        Lt = fmaf(f, s_L[w0 + w], Lt);
+      }
+      float lse_out;
+      if (any_nan) {
+        a = make_float2(NAN, NAN);
+        lse_out = NAN;
+      } else if (M == -INFINITY) {
+        a = make_float2(0.0f, 0.0f);
+        lse_out = -INFINITY;
+      } else {
+        a.x /= Lt;
+        a.y /= Lt;
+        lse_out = M + logf(Lt);
+      }
+      const size_t out_idx = ((size_t)b * hq + h) * mrg::D / 2 + lane;
+      reinterpret_cast<uint32_t*>(merged_o)[out_idx] = mrg::bf16_rne(a.x) | (mrg::bf16_rne(a.y) << 16);
+      if (merged_lse && lane == 0) merged_lse[(size_t)b * hq + h] = lse_out;
+    }
+    __syncthreads();
+  }
+}
+
 template <int G, int W>
 __device__ __forceinline__ void merge_if_last(const float* __restrict__ part_o,
                                               const float* __restrict__ part_lse,
@@ -133,10 +247,7 @@ __device__ __forceinline__ void merge_if_last(const float* __restrict__ part_o,
   }
   __syncthreads();
   if (!s_last) return;
-#pragma unroll 1
-  for (int h = 0; h < G; ++h)
-    mrg::merge_row<true, false, W, true>(part_o, part_lse, merged_o, merged_lse, entries, hq, b,
-                                         g * G + h, nullptr, nullptr, nullptr, 1, 0.0f);
+  merge_group<G, W>(part_o, part_lse, merged_o, merged_lse, b, g, hq, entries);
   if (threadIdx.x == 0)
     __hip_atomic_store(&counters[(size_t)b * hkv + g], 0, __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
