@@ -108,7 +108,8 @@ int qf_attn_decode_split_workspace_size(const qf_decode_desc* desc, size_t* byte
  *               shard's scores (a NaN in V alone poisons only that dim of O).
  *   workspace   device buffer of at least qf_attn_decode_split_workspace_size() bytes, 16-byte
  *               aligned; may be NULL when that size is 0.  Its contents need no initialisation
- *               and are garbage afterwards.
+ *               and are garbage afterwards.  Calls that may run at the same time (other streams)
+ *               need workspaces of their own.
  *   stream      hipStream_t.
  */
 int qf_attn_decode_split(const qf_decode_desc* desc, const void* q, const void* k_cache,
@@ -374,8 +375,8 @@ typedef struct {
  * The sweep beside the feed-forward (§3, "across layers": neither is downstream of the other, so
  * they may run at once): exactly qf_attn_decode_split(desc, q, ..., workspace_size) and
  * qf_linear(*beside), issued as ONE launch whose workgroups take either role, so that on one GPU
- * the two share every CU instead of running one after the other (preceded by the ranking kernel
- * where qf_attn_decode_split ranks the shape's shards).  Results are bitwise those of
+ * the two share every CU instead of running one after the other (preceded by the small kernel
+ * that writes the dispatch order, where qf_attn_decode_split has one).  Results are bitwise those of
  * the two separate calls.  The caller guarantees that neither call's outputs overlap the other's
  * inputs or outputs.  Arguments, errors and ownership are those of the two calls (checked before
  * anything is launched); `beside` is a HOST pointer, read during the call.  With batch == 0 or
