@@ -120,3 +120,43 @@ def test_noalloc_equals_the_workspace_entry_point_on_calls_in_a_row(gpu):
                 _, hi = bf16_neighbours(O[b, h] + delta)
                 assert np.all((o[b, h] >= lo) & (o[b, h] <= hi)), (i, b, h)
                 assert float(np.max(np.abs(o[b, h] - O[b, h]))) <= OUT_ABS
+
+
+@pytest.mark.gpu
+def test_noalloc_replayed_from_a_graph(gpu):
+    """The callers the entry point is for include code under HIP graph capture: captured once
+    (the counter-clearing kernel and the decode), replayed three times with eager calls of another
+    shape on the same scratch array between the replays, every replay equals the eager call
+    bitwise."""
+    import torch
+
+    from parity import say
+    from workloads import make_case
+
+    c = _CALLS[1]
+    case = make_case(c["batch"], c["hq"], c["hkv"], c["ctx"], c["shards"], seed=c["seed"],
+                     device=gpu)
+    B, Hq, D = case.q.shape
+    out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=gpu)
+    lse = torch.empty((B, Hq), dtype=torch.float32, device=gpu)
+    _noalloc_via_abi(case, out, lse)              # eager (and the scratch looked up on this GPU)
+    torch.cuda.synchronize()
+    eager = (out.view(torch.int16).clone(), lse.view(torch.int32).clone())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=torch.cuda.Stream()):
+        _noalloc_via_abi(case, out, lse)          # enqueued on the capturing stream
+    d = _CALLS[3]
+    other = make_case(d["batch"], d["hq"], d["hkv"], d["ctx"], d["shards"], seed=d["seed"],
+                      device=gpu)
+    o2 = torch.empty((1, 16, 128), dtype=torch.bfloat16, device=gpu)
+    l2 = torch.empty((1, 16), dtype=torch.float32, device=gpu)
+    for r in range(3):
+        out.fill_(float("nan"))
+        lse.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        say(f"[noalloc] graph replay {r}")
+        assert torch.equal(out.view(torch.int16), eager[0]), r
+        assert torch.equal(lse.view(torch.int32), eager[1]), r
+        _noalloc_via_abi(other, o2, l2)           # eager use of the same array between replays
+        torch.cuda.synchronize()
