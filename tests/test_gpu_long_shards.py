@@ -257,3 +257,26 @@ def test_long_shards_dispatch_order(gpu):
         live_per_xcd.append(live)
     assert sum(live_per_xcd) == sum(1 for u in range(units) if pages(u) > 0)
     assert min(live_per_xcd[0::2]) >= max(live_per_xcd[1::2]), live_per_xcd
+
+
+@pytest.mark.parametrize("B", [256, 257])
+def test_long_shards_at_the_ordering_limit(gpu, B):
+    """8,192 (request, shard) pairs, the most the ordering kernel ranks (its LDS holds one int32
+    per pair), and one request more, swept in the plain order: the workspace says which, and the
+    sampled outputs meet the oracle's gates either way."""
+    rng = np.random.default_rng(500 + B)
+    n = np.rint(np.exp(rng.uniform(np.log(16), np.log(20000), size=B))).astype(int)
+    n[:3] = [0, 1, 16 * 4096 // 2 + 7]
+    S = np.maximum(1, -(-n // 4096))
+    case = make_case(B, 4, 2, n, S, seed=500 + B, max_shards=32, max_pages=4096, device=gpu)
+    desc = _desc(case)
+    assert qf.split_chunks(desc) == 1
+    ranked = qf.workspace_size(desc) > 0
+    assert ranked == (B * 32 <= 8192)
+    say(f"[long shards] {B} requests, {B * 32} pairs, ranked={ranked}")
+    got = run_gpu(case)
+    order = np.argsort(n)
+    pairs = [(int(b), h) for b in (0, 1, 2, int(order[B // 2]), int(order[-1]), B - 1)
+             for h in (0, 3)]
+    check(case, got, oracle_ref(case, pairs), pairs, label=f"ordering limit B={B}")
+    assert np.all(got["part_lse"][0] == -np.inf)
