@@ -372,8 +372,8 @@ typedef struct {
 } qf_linear_args;
 
 /*
- * The sweep beside the feed-forward (§3, "across layers": neither is downstream of the other, so
- * they may run at once): exactly qf_attn_decode_split(desc, q, ..., workspace_size) and
+ * The sweep beside the feed-forward (§3: the sweep of one layer and the feed-forward of another
+ * do not wait for each other's results, so they may run at once): exactly qf_attn_decode_split(desc, q, ..., workspace_size) and
  * qf_linear(*beside), issued as ONE launch whose workgroups take either role, so that on one GPU
  * the two share every CU instead of running one after the other (preceded by the small kernel
  * that writes the dispatch order, where qf_attn_decode_split has one).  Results are bitwise those of
