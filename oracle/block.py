@@ -16,8 +16,8 @@ Where the paper is silent the Qwen3 blocks it converts fix the form (readings):
   N1, N2 are RMS normalisations with a learned gain, x / sqrt(mean(x^2) + eps) * g, eps = 1e-6;
   M is the SwiGLU feed-forward W_down (silu(W_gate h) * W_up h), silu(x) = x sigmoid(x);
   query head h reads KV head floor(h / G) (grouped-query attention);
-  the key reads z as §2 states it (§8's "scoring from x" names the query's side; §8 also notes
-  that where the key is read is free for the sweep);
+  the key reads z as §2 states it (in §8's A_{x;z} the scores come from x, which names the
+  query's side; §8 also notes that where the key is read is free for the sweep);
   rotary position embeddings and Qwen3's per-head q/k normalisation are left out (they act on q
   and k elementwise and do not bear on which point of the stream each reads).
 
