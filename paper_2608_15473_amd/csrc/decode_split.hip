@@ -48,14 +48,7 @@ __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
                                          __builtin_bit_cast(bf16x2_t, b), c, false);
 }
 
-// Sum over the 16 lanes of a DPP row; the result is bitwise identical on all 16 lanes.
-__device__ __forceinline__ float row_sum16(float x) {
-  x += __builtin_amdgcn_update_dpp(0.0f, x, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
-  x += __builtin_amdgcn_update_dpp(0.0f, x, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
-  x += __builtin_amdgcn_update_dpp(0.0f, x, 0x141, 0xF, 0xF, false);  // row_half_mirror
-  x += __builtin_amdgcn_update_dpp(0.0f, x, 0x140, 0xF, 0xF, false);  // row_mirror
-  return x;
-}
+using mrg::row_sum16;  // sum over the 16 lanes of a DPP row, the same bits on each
 
 // Lane 4*(c/4) + h's value in every lane c of its quad (DPP quad_perm [h,h,h,h]).
 __device__ __forceinline__ float quad_bcast(float x, int h) {
@@ -120,8 +113,8 @@ __device__ __forceinline__ void unpack8(const uint4& w, float* f) {
 // of the group.  When one 16-slot group per wavefront covers the slots with W / G wavefronts per
 // head (or W / 2, ...), heads are merged side by side by teams of wavefronts, and every wavefront
 // loads its log-partitions and O rows at once (one memory round trip; the O rows of empty slots
-// are read and discarded); each team sums exactly what merge_row's wavefronts sum, in the same
-// order, so the bits are merge_row's.  Otherwise head by head with merge_row.  The partial states
+// are read and discarded); each team sums exactly what merge_row's wavefronts sum, with the same
+// code (mrg::WaveMerge), so the bits are merge_row's.  Otherwise head by head with merge_row.  The partial states
 // were written by other workgroups of this launch: read with device-scope loads.
 template <int G, int W>
 __device__ __forceinline__ void merge_group(const float* __restrict__ part_o,
@@ -129,7 +122,7 @@ __device__ __forceinline__ void merge_group(const float* __restrict__ part_o,
                                             uint16_t* __restrict__ merged_o,
                                             float* __restrict__ merged_lse, int b, int g, int hq,
                                             int entries) {
-  constexpr int K = 16;
+  constexpr int K = mrg::K;
   const int groups = (entries + K - 1) / K;
   const int hpw = min(G, W / max(groups, 1));   // heads merged side by side
   if (hpw < 2) {
@@ -143,85 +136,37 @@ __device__ __forceinline__ void merge_group(const float* __restrict__ part_o,
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int sub = wave / wph, wl = wave % wph;
-  __shared__ float2 s_acc[W][64];
-  __shared__ float s_L[W];
-  __shared__ float s_m[W];
-  __shared__ int s_nan[W];
+  const bool in_team = sub < hpw;
+  const int i0 = K * wl;
+  __shared__ mrg::WaveMergeLds<W> lds;
 #pragma unroll 1
   for (int h0 = 0; h0 < G; h0 += hpw) {
     const int h = g * G + h0 + min(sub, hpw - 1);
     const float* lse = part_lse + (size_t)b * entries * hq + h;
     const float* o = part_o + ((size_t)b * entries * hq + h) * mrg::D + 2 * lane;
-    const size_t o_step = (size_t)hq * mrg::D;
-    float x[K];
-    uint64_t raw[K];
+    const int32_t o_step = hq * mrg::D;
+    const float* o_i0 = o + (size_t)i0 * o_step;
+    float x = -INFINITY;
+    if (in_team && lane < K && i0 + lane < entries)
+      x = __hip_atomic_load(&lse[(size_t)(i0 + lane) * hq], __ATOMIC_RELAXED,
+                            __HIP_MEMORY_SCOPE_AGENT);
+    float2 v[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) {
-      const int i = K * wl + k;
-      const bool in = sub < hpw && i < entries;
-      x[k] = in ? __hip_atomic_load(&lse[(size_t)i * hq], __ATOMIC_RELAXED,
-                                    __HIP_MEMORY_SCOPE_AGENT)
-                : -INFINITY;
-      raw[k] = in ? __hip_atomic_load(reinterpret_cast<const uint64_t*>(o + i * o_step),
-                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                  : 0ull;
+      const bool in = in_team && i0 + k < entries;
+      v[k] = __builtin_bit_cast(
+          float2, in ? __hip_atomic_load(reinterpret_cast<const uint64_t*>(o_i0 + k * o_step),
+                                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                     : 0ull);
     }
     // This wavefront's group, as one round of merge_row's loop.
-    float m_w = -INFINITY, L = 0.0f;
-    float2 acc = make_float2(0.0f, 0.0f);
-    bool nan = false;
-    float mc = -INFINITY;
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-      nan |= (x[k] != x[k]);
-      mc = fmaxf(mc, x[k]);
-    }
-    if (mc != -INFINITY) {
-      m_w = mc;
-#pragma unroll
-      for (int k = 0; k < K; ++k) {
-        const float w = (x[k] == -INFINITY) ? 0.0f : expf(x[k] - m_w);
-        const float2 v = __builtin_bit_cast(float2, raw[k]);
-        L += w;
-        acc.x = (w == 0.0f) ? acc.x : fmaf(w, v.x, acc.x);
-        acc.y = (w == 0.0f) ? acc.y : fmaf(w, v.y, acc.y);
-      }
-    }
-    s_acc[wave][lane] = acc;
-    if (lane == 0) {
-      s_L[wave] = L;
-      s_m[wave] = m_w;
-      s_nan[wave] = nan;
-    }
+    mrg::WaveMerge st;
+    st.add(x, v);
+    lds.put(wave, lane, st);
     __syncthreads();
-    if (sub < hpw && wl == 0) {   // the team's first wavefront: merge_row's final merge
-      const int w0 = sub * wph;
-      float M = s_m[w0];
-      bool any_nan = s_nan[w0];
-      for (int w = 1; w < wph; ++w) {
-        M = fmaxf(M, s_m[w0 + w]);
-        any_nan |= s_nan[w0 + w];
-      }
-      float2 a = make_float2(0.0f, 0.0f);
-      float Lt = 0.0f;
-      for (int w = 0; w < wph; ++w) {
-        const float f = (s_m[w0 + w] == -INFINITY) ? 0.0f : expf(s_m[w0 + w] - M);
-        a.x = fmaf(f, s_acc[w0 + w][lane].x, a.x);
-        a.y = fmaf(f, s_acc[w0 + w][lane].y, a.y);
-        Lt = fmaf(f, s_L[w0 + w], Lt);
-      }
+    if (in_team && wl == 0) {   // the team's first wavefront: merge_row's final merge
       float lse_out;
-      if (any_nan) {
-        a = make_float2(NAN, NAN);
-        lse_out = NAN;
-      } else if (M == -INFINITY) {
-        a = make_float2(0.0f, 0.0f);
-        lse_out = -INFINITY;
-      } else {
-        a.x /= Lt;
-        a.y /= Lt;
-        lse_out = M + logf(Lt);
-      }
+      const float2 a = lds.finish(sub * wph, wph, lane, lse_out);
       const size_t out_idx = ((size_t)b * hq + h) * mrg::D / 2 + lane;
       reinterpret_cast<uint32_t*>(merged_o)[out_idx] = mrg::bf16_rne(a.x) | (mrg::bf16_rne(a.y) << 16);
       if (merged_lse && lane == 0) merged_lse[(size_t)b * hq + h] = lse_out;
