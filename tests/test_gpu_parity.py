@@ -291,6 +291,30 @@ def test_combine_selects_empty_slots_and_propagates_nan(gpu):
     assert np.all(np.isnan(out[1, 1])) and np.isnan(lse[1, 1])
 
 
+@pytest.mark.parametrize("live", [5, 16, 24])
+def test_combine_bits_do_not_depend_on_appended_empty_slots(gpu, live):
+    """Empty slots appended behind the live ones (ln Z = -inf, O garbage) change no bit of the
+    merge as long as one round of 16 slots per wavefront covers the row: the workgroup grows from
+    1 to 16 wavefronts with the slot count, every wavefront sums the same live slots, and empty
+    ones add exact zeros."""
+    B, Hq, D = 3, 8, 128
+    rng = np.random.default_rng(40 + live)
+    po = rng.standard_normal((B, live, Hq, D)).astype(np.float32)
+    pl = (rng.standard_normal((B, live, Hq)) * 30 + 50).astype(np.float32)
+    pl[1, ::3, 2] = -np.inf                   # some empty slots among the live ones
+    ref_out, ref_lse = qf.attn_combine(torch.from_numpy(po).to(gpu), torch.from_numpy(pl).to(gpu))
+    for total in sorted({live + 1, 32, 64, 128, 200, 256}):
+        if total <= live:
+            continue
+        po2 = np.full((B, total, Hq, D), np.nan, dtype=np.float32)
+        pl2 = np.full((B, total, Hq), -np.inf, dtype=np.float32)
+        po2[:, :live], pl2[:, :live] = po, pl
+        out, lse = qf.attn_combine(torch.from_numpy(po2).to(gpu), torch.from_numpy(pl2).to(gpu))
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), ref_out.view(torch.int16)), total
+        assert torch.equal(lse.view(torch.int32), ref_lse.view(torch.int32)), total
+
+
 # ------------------------------------------------------------------------------------------------
 # full-size workloads: one layer at its real shape, sampled outputs
 # ------------------------------------------------------------------------------------------------
