@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define QF_VERSION 7
+#define QF_VERSION 8
 
 #define QF_OK 0
 #define QF_EINVAL (-1)       /* null pointer, negative or inconsistent size, Hq % Hkv != 0   */
@@ -55,10 +55,14 @@ extern "C" {
 #define QF_EALIGN (-3)       /* a pointer is not aligned as documented below                 */
 #define QF_EHIP (-4)         /* the HIP runtime refused a launch; message from hipGetErrorString */
 
+/* Upper bound on the query heads Hq of every call (the merge kernels address one round of 16 slots
+ * of a row with 32-bit offsets); larger values are rejected with QF_EINVAL. */
+#define QF_MAX_Q_HEADS 4096
+
 /* Shape of one decode step.  Every field is a host value. */
 typedef struct qf_decode_desc {
   int32_t batch;             /* B  >= 0 requests (B == 0: the calls do nothing)               */
-  int32_t n_q_heads;         /* Hq >= 1 query heads                                           */
+  int32_t n_q_heads;         /* Hq query heads, 1 <= Hq <= QF_MAX_Q_HEADS                     */
   int32_t n_kv_heads;        /* Hkv >= 1 KV heads; G = Hq / Hkv query heads share one KV head */
   int32_t head_dim;          /* D, must be 128                                                */
   int32_t page_size;         /* P, positions per cache page, must be 16                       */
@@ -230,7 +234,7 @@ int qf_attn_decode_noalloc(const qf_decode_desc* desc, const void* q, const void
  *   out         bf16 [B, Hq, D], 4-byte aligned; round-to-nearest-even.  All slots empty
  *               (n_b = 0): +0.  A NaN log-sum-exp among the slots: NaN.
  *   lse         fp32 [B, Hq] natural log, or NULL if not wanted.  All empty: -inf.
- *   head_dim must be 128.
+ *   head_dim must be 128; 1 <= n_q_heads <= QF_MAX_Q_HEADS.
  */
 int qf_attn_combine(int32_t batch, int32_t n_q_heads, int32_t head_dim, int32_t max_shards,
                     const float* part_out, const float* part_lse, void* out, float* lse,
@@ -249,7 +253,8 @@ int qf_attn_combine(int32_t batch, int32_t n_q_heads, int32_t head_dim, int32_t 
  *   q           bf16 [B, Hq, D] (the same query the sweep used), 4-byte aligned.
  *   k_cur,v_cur bf16 [B, Hkv, D]: the current token's key and value; query head h uses KV head
  *               h / G.  4-byte aligned.
- *   part_out, part_lse, out, lse as for qf_attn_combine.  head_dim must be 128.
+ *   part_out, part_lse, out, lse as for qf_attn_combine.  head_dim must be 128;
+ *   1 <= n_q_heads <= QF_MAX_Q_HEADS.
  */
 int qf_attn_combine_current(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
                             int32_t max_shards, const float* part_out, const float* part_lse,

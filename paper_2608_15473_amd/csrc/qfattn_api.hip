@@ -45,6 +45,8 @@ int check_desc(const qf_decode_desc* d) {
   if (d->batch < 0) return fail(QF_EINVAL, "batch %d < 0", d->batch);
   if (d->n_q_heads < 1 || d->n_kv_heads < 1)
     return fail(QF_EINVAL, "n_q_heads %d / n_kv_heads %d must be >= 1", d->n_q_heads, d->n_kv_heads);
+  if (d->n_q_heads > QF_MAX_Q_HEADS)
+    return fail(QF_EINVAL, "n_q_heads %d > %d", d->n_q_heads, QF_MAX_Q_HEADS);
   if (d->n_q_heads % d->n_kv_heads != 0)
     return fail(QF_EINVAL, "n_q_heads %d is not a multiple of n_kv_heads %d", d->n_q_heads,
                 d->n_kv_heads);
@@ -455,7 +457,8 @@ int qf_attn_combine(int32_t batch, int32_t n_q_heads, int32_t head_dim, int32_t 
                     void* stream) {
   g_error[0] = 0;
   if (batch < 0) return fail(QF_EINVAL, "batch %d < 0", batch);
-  if (n_q_heads < 1) return fail(QF_EINVAL, "n_q_heads %d < 1", n_q_heads);
+  if (n_q_heads < 1 || n_q_heads > QF_MAX_Q_HEADS)
+    return fail(QF_EINVAL, "n_q_heads %d not in [1, %d]", n_q_heads, QF_MAX_Q_HEADS);
   if (max_shards < 1) return fail(QF_EINVAL, "max_shards %d < 1", max_shards);
   if (head_dim != qf::kHeadDim) return fail(QF_EUNSUPPORTED, "head_dim %d != %d", head_dim, qf::kHeadDim);
   if (batch == 0) return QF_OK;
@@ -485,6 +488,8 @@ int qf_attn_combine_current(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads
   if (batch < 0) return fail(QF_EINVAL, "batch %d < 0", batch);
   if (n_q_heads < 1 || n_kv_heads < 1)
     return fail(QF_EINVAL, "n_q_heads %d / n_kv_heads %d must be >= 1", n_q_heads, n_kv_heads);
+  if (n_q_heads > QF_MAX_Q_HEADS)
+    return fail(QF_EINVAL, "n_q_heads %d > %d", n_q_heads, QF_MAX_Q_HEADS);
   if (n_q_heads % n_kv_heads != 0)
     return fail(QF_EINVAL, "n_q_heads %d is not a multiple of n_kv_heads %d", n_q_heads, n_kv_heads);
   if (max_shards < 1) return fail(QF_EINVAL, "max_shards %d < 1", max_shards);

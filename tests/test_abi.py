@@ -58,6 +58,7 @@ def _ws(desc):
 @pytest.mark.parametrize("kw,code", [
     (dict(batch=-1), qf.QF_EINVAL),
     (dict(n_q_heads=0), qf.QF_EINVAL),
+    (dict(n_q_heads=8192, n_kv_heads=1024), qf.QF_EINVAL),     # above QF_MAX_Q_HEADS
     (dict(n_q_heads=12, n_kv_heads=8), qf.QF_EINVAL),
     (dict(n_q_heads=48, n_kv_heads=3), qf.QF_EUNSUPPORTED),
     (dict(n_q_heads=32, n_kv_heads=2), qf.QF_EUNSUPPORTED),
@@ -209,6 +210,7 @@ def test_combine_rejects_bad_arguments():
     a = ctypes.c_void_p(4096)
     assert lib.qf_attn_combine(-1, 16, 128, 4, a, a, a, a, None) == qf.QF_EINVAL
     assert lib.qf_attn_combine(2, 0, 128, 4, a, a, a, a, None) == qf.QF_EINVAL
+    assert lib.qf_attn_combine(2, 4097, 128, 4, a, a, a, a, None) == qf.QF_EINVAL
     assert lib.qf_attn_combine(2, 16, 64, 4, a, a, a, a, None) == qf.QF_EUNSUPPORTED
     assert lib.qf_attn_combine(2, 16, 128, 0, a, a, a, a, None) == qf.QF_EINVAL
     assert lib.qf_attn_combine(2, 16, 128, 4, None, a, a, a, None) == qf.QF_EINVAL
@@ -222,6 +224,7 @@ def test_current_token_entry_points_reject_bad_arguments():
     f = lib.qf_attn_combine_current
     assert f(-1, 16, 8, 128, 4, a, a, a, a, a, 0.1, a, a, None) == qf.QF_EINVAL
     assert f(2, 16, 6, 128, 4, a, a, a, a, a, 0.1, a, a, None) == qf.QF_EINVAL
+    assert f(2, 8192, 1024, 128, 4, a, a, a, a, a, 0.1, a, a, None) == qf.QF_EINVAL
     assert f(2, 16, 8, 64, 4, a, a, a, a, a, 0.1, a, a, None) == qf.QF_EUNSUPPORTED
     assert f(2, 16, 8, 128, 4, a, a, None, a, a, 0.1, a, a, None) == qf.QF_EINVAL
     assert f(2, 16, 8, 128, 4, a, a, a, a, a, float("inf"), a, a, None) == qf.QF_EINVAL
