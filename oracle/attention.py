@@ -19,7 +19,7 @@ numpy's own reductions; nothing is blocked, fused or reordered beyond what the d
 
 Parity status: every function here is pinned by ``tests/test_oracle_pins.py`` (closed forms,
 invariants, brute force, library special cases, the paper's split experiment).  The paper's
-worked example of a 400-position shard at "score spread 30" (Appendix A) is NOT reproduced by any
+worked example of a 400-position shard whose scores spread over 30 nats (Appendix A) is NOT reproduced by any
 reading of it and is therefore not used as a pin (parity unpinned for that example only).
 """
 
