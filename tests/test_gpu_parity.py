@@ -315,6 +315,27 @@ def test_combine_bits_do_not_depend_on_appended_empty_slots(gpu, live):
         assert torch.equal(lse.view(torch.int32), ref_lse.view(torch.int32)), total
 
 
+@pytest.mark.parametrize("slots", [40, 300])
+def test_combine_at_the_query_head_limit(gpu, slots):
+    """QF_MAX_Q_HEADS query heads, one round of slots (40) and two (300, past 16 wavefronts of 16):
+    the merge of a head reads only that head's slots, so every head equals a combine of its own
+    8-head slice, bitwise; and one head above the limit is refused before any launch."""
+    B, Hq, D = 1, 4096, 128
+    g = torch.Generator(device=gpu).manual_seed(300 + slots)
+    po = torch.randn(B, slots, Hq, D, generator=g, device=gpu)
+    pl = torch.randn(B, slots, Hq, generator=g, device=gpu) * 20 + 40
+    pl[:, ::7, 2000:2100] = -float("inf")
+    out, lse = qf.attn_combine(po, pl)
+    for h0 in (0, 2048, 4088):
+        o8, l8 = qf.attn_combine(po[:, :, h0:h0 + 8].contiguous(), pl[:, :, h0:h0 + 8].contiguous())
+        torch.cuda.synchronize()
+        assert torch.equal(out[:, h0:h0 + 8].view(torch.int16), o8.view(torch.int16)), h0
+        assert torch.equal(lse[:, h0:h0 + 8].view(torch.int32), l8.view(torch.int32)), h0
+    with pytest.raises(qf.QFError):
+        qf.attn_combine(torch.zeros(1, 1, Hq + 1, D, device=gpu),
+                        torch.zeros(1, 1, Hq + 1, device=gpu))
+
+
 # ------------------------------------------------------------------------------------------------
 # full-size workloads: one layer at its real shape, sampled outputs
 # ------------------------------------------------------------------------------------------------
