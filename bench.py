@@ -482,10 +482,12 @@ def main():
     torch.cuda.synchronize()
 
     # The sweep's launch duration is timed with HIP events on a sample of the timed region's
-    # launches: every EVERY-th sweep (one layer per step for a model of 8+ layers, every 8th step
-    # otherwise).  Events around every launch would add their host cost to each step, which on the
-    # launch-bound workloads (one small layer, the per-GPU share) is most of a step's host time.
-    EVERY = L if L >= 8 else 8
+    # launches: every EVERY-th sweep (one layer per step for a model of 8+ layers; for fewer
+    # layers every 8th to 64th step, at least ~32 launches in all).  Events around every launch
+    # would add their cost to each step, which on the launch-bound workloads (one small layer, the
+    # per-GPU share) is a large part of a step: on the small single layer one pair per 8 steps
+    # still added ~0.7 us to an ~11 us step.
+    EVERY = L
     launches = [0]
 
     def step(events=None):
@@ -511,17 +513,34 @@ def main():
                 plans[(base + l) % copies].combine()
 
     with torch.cuda.stream(run_stream):
+        # Warm-up: the same steps back to back, so that the GPU is busy throughout and reaches
+        # its steady clocks before the timed region.  Without --warmup: three synchronized steps
+        # estimate the step time, then back-to-back steps for >= WARMUP_SECONDS, synchronized
+        # after every ~10 ms of work so that the host never runs far ahead of the GPU.  (A
+        # synchronization after every warm-up step left the GPU idle between steps, and the small
+        # single layer then timed ~15 us per step instead of ~11.)
         warm, t_w = 0, time.perf_counter()
-        while (warm < args.warmup) if args.warmup is not None else \
-                (warm < 3 or time.perf_counter() - t_w < WARMUP_SECONDS):
-            step()
-            warm += 1
-            if args.warmup is None:
+        if args.warmup is not None:
+            for _ in range(args.warmup):
+                step()
+            warm = args.warmup
+        else:
+            for _ in range(3):
+                step()
                 torch.cuda.synchronize()
+            warm = 3
+            batch = max(1, int(0.01 * warm / max(time.perf_counter() - t_w, 1e-6)))
+            while time.perf_counter() - t_w < WARMUP_SECONDS:
+                for _ in range(batch):
+                    step()
+                torch.cuda.synchronize()
+                warm += batch
         torch.cuda.synchronize()
         per_step = (time.perf_counter() - t_w) / max(1, warm)
         if args.steps is None:
             args.steps = max(10, int(TIMED_SECONDS / max(per_step, 1e-6)) + 1)
+        if L < 8:
+            EVERY = max(8, min(64, args.steps // 32)) * L
         args.warmup = warm
         log(f"[bench] warmup done ({warm} steps); timing {args.steps} steps")
         ev = []
